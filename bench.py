@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Throughput of the fused V-trace loss+grad step on one MI355X.
+
+One step is one vtrace_loss_grad call over a whole [T, B] batch: both
+log-softmaxes, the importance weights, the reverse V-trace recursion, the
+advantages, the three losses and the gradients w.r.t. logits and values.
+Inputs are generated once, uploaded, and stay resident in HBM; the timed region
+holds K back-to-back calls.  Prints one JSON line on stdout.
+
+Default workload: the stress batch, T=1000, B=16384, A=18, fp32 logits,
+rho_bar = c_bar = lambda = 1 (3.87 GB of algorithmic traffic per step, far
+beyond the 256 MB Infinity Cache, so no cache flush is needed between steps).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, AMD's published peak
+METRIC = "trajectory steps/sec (T*B) for fused V-trace loss+grad; achieved HBM GB/s"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "loss_grad_stress_counters.json")
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=4, help="synthetic workload id (0-4)")
+    ap.add_argument("--params", type=int, default=0, help="parameter set of the workload")
+    ap.add_argument("--bf16", action="store_true", help="bfloat16 logits")
+    ap.add_argument("--kernel", choices=["auto", "lane_serial"], default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time for the oracle baseline sample")
+    return ap.parse_args()
+
+
+def kernel_source_digest() -> str:
+    """Hash of the HIP sources, to tell whether stored counters still describe them."""
+    csrc = os.path.join(ROOT, "paper_1802_01561_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(f.encode())
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(T, B, A, logit_bytes):
+    """Bytes one call must move: both logit rows, action, reward, discount and
+    value in; d_logits (fp32) and d_values out; plus the bootstrap values."""
+    per_step = 2 * A * logit_bytes + 16 + 4 * A + 4
+    return T * B * per_step + 4 * B, per_step
+
+
+def to_device(tr, torch, np):
+    zt, yt = tr.logits_for_device()
+    if tr.dtype == "bf16":
+        z = torch.from_numpy(zt.view(np.int16)).view(torch.bfloat16)
+        y = torch.from_numpy(yt.view(np.int16)).view(torch.bfloat16)
+    else:
+        z, y = torch.from_numpy(zt), torch.from_numpy(yt)
+    d = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    return dict(target_logits=z.cuda(), behaviour_logits=y.cuda(), actions=d(tr.actions),
+                rewards=d(tr.rewards), discounts=d(tr.discounts), values=d(tr.values),
+                bootstrap_value=d(tr.bootstrap_value))
+
+
+def stored_traffic(per_launch_kernel_ms):
+    """HBM bytes per launch from committed rocprofv3 counter runs, or None when
+    they are missing or were taken on different kernel sources."""
+    try:
+        with open(COUNTERS_FILE) as fh:
+            c = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if c.get("kernel_source_digest") != kernel_source_digest():
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(tr, p, target_s):
+    """The fp64 oracle on a bounded sample of lanes (all T), on one host thread."""
+    import numpy as np
+    import oracle
+    from synth import subset_lanes
+
+    def run(n):
+        sub = subset_lanes(tr, np.arange(n))
+        t0 = time.perf_counter()
+        oracle.loss_and_grads(sub.target_logits, sub.behaviour_logits, sub.actions, sub.rewards,
+                              sub.discounts, sub.values, sub.bootstrap_value, p.rho_bar, p.c_bar,
+                              p.lam, p.baseline_cost, p.entropy_cost)
+        return time.perf_counter() - t0
+
+    n0 = min(tr.B, 64)
+    t0 = run(n0)
+    n = int(min(tr.B, max(n0, n0 * target_s / max(t0, 1e-6))))
+    wall = run(n)
+    cpu_model = platform.processor()
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {
+        "value": tr.T * n / wall,
+        "unit": "steps/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{n} of {tr.B} lanes x all T={tr.T} steps ({tr.T * n} steps), "
+                  f"fp64 NumPy, one thread, {wall:.1f} s wall",
+        "cpu_model": cpu_model,
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path. Lanes are "
+              "independent, so the batch axis would shard across GPUs with no communication "
+              "except a 4-float loss all-reduce.", file=sys.stderr)
+        sys.exit(2)
+    if args.kernel == "lane_serial":
+        os.environ["VTRACE_KERNEL"] = "lane_serial"
+
+    import numpy as np
+    import torch
+
+    import paper_1802_01561_amd as vt
+    from synth import PARAM_SETS, make_config
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+
+    t_gen = time.perf_counter()
+    tr = make_config(args.config, bf16=args.bf16)
+    p = PARAM_SETS[args.config][args.params]
+    dev = to_device(tr, torch, np)
+    T, B, A = tr.T, tr.B, tr.A
+    print(f"[bench] {tr.name} T={T} B={B} A={A} {tr.dtype} {p.label()} "
+          f"(generated+uploaded in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+
+    ws = vt.Workspace(T, B, A)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    out = vt.LossGrad(torch.empty(4, **f32), torch.empty((T, B, A), **f32),
+                      torch.empty((T, B), **f32), None, None, None)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                            baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
+                            workspace=ws, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    kernel_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    ms_per_step = (t1 - t0) * 1e3 / K
+    steps_per_s = T * B / (ms_per_step * 1e-3)
+    logit_bytes = 2 if args.bf16 else 4
+    alg_bytes, per_step = algorithmic_bytes(T, B, A, logit_bytes)
+    avg_kernel_ms = float(kernel_ms.mean())
+    achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
+    losses = out.losses.cpu().tolist()
+    print(f"[bench] kernel avg {avg_kernel_ms:.4f} ms (min {kernel_ms.min():.4f}, median "
+          f"{np.median(kernel_ms):.4f}); wall {ms_per_step:.4f} ms/step; {achieved:.1f} GB/s "
+          f"algorithmic; losses {losses}", file=sys.stderr, flush=True)
+
+    traffic = stored_traffic(avg_kernel_ms)
+    result = {
+        "metric": METRIC,
+        "value": steps_per_s,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-in/f32" if args.bf16 else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{tr.name}: T={T} B={B} A={A} {tr.dtype} logits, "
+                        f"rho_bar={p.rho_bar} c_bar={p.c_bar} lambda={p.lam}",
+            "T": T, "B": B, "A": A, "logits": tr.dtype,
+            "rho_bar": p.rho_bar if math.isfinite(p.rho_bar) else "inf",
+            "c_bar": p.c_bar if math.isfinite(p.c_bar) else "inf",
+            "lambda": p.lam, "baseline_cost": p.baseline_cost, "entropy_cost": p.entropy_cost,
+            "seed": tr.seed,
+        },
+        "kernel_ms_avg": avg_kernel_ms,
+        "kernel_ms_min": float(kernel_ms.min()),
+        "alg_bytes_per_step": per_step,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(tr, p, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

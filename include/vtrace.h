@@ -1,0 +1,184 @@
+/*
+ * libvtrace: the learner-side V-trace actor-critic step of IMPALA
+ * (Espeholt et al., 2018, "IMPALA: Scalable Distributed Deep-RL with Importance
+ * Weighted Actor-Learner Architectures"), on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI.  Every array argument is a DEVICE pointer owned by the caller; the
+ * library allocates nothing and keeps no global mutable state.  Each call
+ * validates its arguments on the host, enqueues its kernel(s) on `stream`
+ * (NULL = the null stream) and returns without synchronising.  A returned
+ * VTRACE_OK means the arguments were valid and the launch was accepted; device
+ * faults surface on the caller's next synchronisation.
+ *
+ * Layout.  Batches are time-major and row-major: element (t, b) of a [T,B] array
+ * is at index t*B + b, and element (t, b, j) of a [T,B,A] array at
+ * (t*B + b)*A + j, the action axis innermost (the learner folds time into the
+ * batch, paper Sec. 3.1).
+ *
+ * Inputs (shared by vtrace_targets and vtrace_loss_grad):
+ *   target_logits     [T,B,A]  logits of the learner policy pi, dtype `logits_dtype`
+ *   behaviour_logits  [T,B,A]  logits of the actor policy mu the actions were drawn from
+ *   actions           [T,B]    int32, 0 <= a < A
+ *   rewards           [T,B]    float32, r_t
+ *   discounts         [T,B]    float32, gamma_t: discount between x_t and x_{t+1};
+ *                              0 marks an episode that ended after step t
+ *   values            [T,B]    float32, V(x_t)
+ *   bootstrap_value   [B]      float32, V(x_T)
+ *   rho_bar, c_bar             truncation levels of Sec. 4.1; >= 0, +INFINITY allowed
+ *                              (no truncation).  rho_bar < c_bar is accepted.
+ *   lambda                     trace discount of Remark 2, in [0, 1]; scales c only.
+ *
+ * Definitions computed (Sec. 4.1, Eq. (1), Remarks 1-2, Sec. 4.2):
+ *   ratio_t = pi(a_t|x_t) / mu(a_t|x_t)             (from the two log-softmaxes)
+ *   rho_t   = min(rho_bar, ratio_t)
+ *   c_t     = lambda * min(c_bar, ratio_t)
+ *   delta_t = rho_t (r_t + gamma_t V(x_{t+1}) - V(x_t)),  V(x_T) = bootstrap_value
+ *   v_s     = V(x_s) + sum_{t=s}^{T-1} (gamma_s..gamma_{t-1})(c_s..c_{t-1}) delta_t
+ *             (every v_s uses the rest of the unroll; v_T = V(x_T))
+ *   pg_adv_s = rho_s (r_s + gamma_s v_{s+1} - V(x_s))
+ *
+ * Numerics.  Per-row softmax work is float32; the importance ratio is formed
+ * in float64 from the float32 exponent sums, and the recursion, advantages and
+ * loss partial sums are float64.  Outputs are float32.  NaN or Inf inputs are
+ * propagated, not sanitised.
+ *
+ * Errors that only the device can see.  An action outside [0, A) makes that
+ * step's importance ratio NaN; the NaN reaches that step's outputs, every
+ * earlier step of the same lane, and the policy-gradient, baseline and total
+ * losses (the entropy loss does not depend on actions).  When a workspace is
+ * passed the kernel also raises a sticky flag in it (vtrace_error_flag).
+ *
+ * Outputs must not alias inputs or each other.  Base pointers of logits,
+ * d_logits and gathered arrays must be 16-byte aligned; all others 4-byte.
+ * Calls are re-entrant; concurrent calls need distinct workspaces.
+ */
+#ifndef VTRACE_H_
+#define VTRACE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t* vtrace_stream_t;
+
+typedef enum {
+  VTRACE_OK = 0,
+  VTRACE_ERR_NULL = 1,      /* a required pointer is NULL */
+  VTRACE_ERR_SHAPE = 2,     /* T, B or A < 1, or T*B*A beyond the supported range */
+  VTRACE_ERR_DTYPE = 3,     /* unknown logits dtype */
+  VTRACE_ERR_PARAM = 4,     /* NaN or out-of-range scalar parameter */
+  VTRACE_ERR_ALIGN = 5,     /* a base pointer breaks the alignment rule above */
+  VTRACE_ERR_WORKSPACE = 6, /* workspace NULL or smaller than vtrace_workspace_bytes */
+  VTRACE_ERR_HIP = 7        /* the HIP runtime rejected the launch */
+} vtrace_status;
+
+typedef enum {
+  VTRACE_F32 = 0,  /* IEEE binary32 logits */
+  VTRACE_BF16 = 1  /* bfloat16 logits (upper half of a binary32) */
+} vtrace_dtype;
+
+/* Version of this interface; bumped on any incompatible change. */
+int vtrace_abi_version(void);
+
+/* Static, never-NULL description of a status code. */
+const char* vtrace_status_string(vtrace_status s);
+
+/* Largest T*B*A the kernels accept. */
+int64_t vtrace_max_elements(void);
+
+/*
+ * Bytes of device workspace that vtrace_loss_grad needs for a [T,B,A] batch
+ * (the cross-workgroup loss partials, a completion counter and the error
+ * flag).  Returns 0 for invalid sizes.
+ */
+size_t vtrace_workspace_bytes(int64_t T, int64_t B, int64_t A);
+
+/*
+ * Clears a workspace (counter, error flag, partials) with a fill kernel on
+ * `stream`.  Call once after allocating it; vtrace_loss_grad leaves the counter
+ * at zero again after every call, so a workspace can be reused without clearing.
+ */
+vtrace_status vtrace_workspace_init(void* workspace, size_t workspace_bytes,
+                                    vtrace_stream_t stream);
+
+/*
+ * V-trace targets and policy-gradient advantages (Sec. 4.1, Eq. (1), Remark 1;
+ * Sec. 4.2 for pg_adv).
+ *   vs, pg_advantages  [T,B] float32 outputs (both required)
+ *   workspace          optional (may be NULL, then workspace_bytes is ignored):
+ *                      when given, receives the out-of-range-action flag.
+ */
+vtrace_status vtrace_targets(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* values,
+    const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
+    float* vs, float* pg_advantages,
+    void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
+
+/*
+ * The V-trace actor-critic losses and their gradients (Sec. 4.2), fused with the
+ * targets into one pass over the batch.
+ *
+ * Losses, summed over batch and time (paper App. D: "the loss is summed across
+ * the batch and time dimensions"):
+ *   policy gradient  L_pg  = -sum pg_adv_s * log pi(a_s|x_s)
+ *   baseline         L_v   = baseline_cost * 1/2 * sum (v_s - V(x_s))^2
+ *   entropy          L_ent = entropy_cost * sum_s sum_a pi(a|x_s) log pi(a|x_s)
+ * Descending these moves along the paper's three update directions: the
+ * importance-weighted policy gradient, the value direction (v_s - V)grad V and
+ * the entropy bonus.  The paper's settings are baseline_cost = 0.5 and
+ * entropy_cost = 0.01 (App. D).  rho, c, v_s and pg_adv are targets: no gradient
+ * flows through them, and none reaches behaviour_logits or bootstrap_value.
+ *
+ *   baseline_cost, entropy_cost  finite floats
+ *   losses        [4] float32 device: {L_pg + L_v + L_ent, L_pg, L_v, L_ent}
+ *   d_logits      [T,B,A] float32: dL/d target_logits
+ *                 = pg_adv_t (pi_j - 1[j = a_t]) + entropy_cost pi_j (log pi_j + H_t),
+ *                 H_t = -sum_j pi_j log pi_j
+ *   d_values      [T,B] float32: dL/dV(x_t) = baseline_cost (V(x_t) - v_t)
+ *   vs, pg_advantages  optional [T,B] float32 outputs (NULL to skip)
+ *   lane_losses   optional [B,3] float32: per-lane {L_pg, L_v, L_ent} over time
+ *   workspace     required, >= vtrace_workspace_bytes(T,B,A) bytes, cleared once
+ *                 by vtrace_workspace_init.
+ * The loss totals are reduced in a fixed order: repeated calls on the same
+ * inputs give bit-identical results.
+ */
+vtrace_status vtrace_loss_grad(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* values,
+    const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
+    float baseline_cost, float entropy_cost,
+    float* losses, float* d_logits, float* d_values,
+    float* vs, float* pg_advantages, float* lane_losses,
+    void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
+
+/*
+ * Copies of the logits at the taken actions: gathered[t,b,0] = target_logits[t,b,a_t]
+ * and gathered[t,b,1] = behaviour_logits[t,b,a_t], bit for bit, in the logits
+ * dtype ([T,B,2]).  These are the pi(a_t|x_t) and mu(a_t|x_t) lookups of
+ * Sec. 4.1 before normalisation.  Out-of-range actions give all-ones bit
+ * patterns (a NaN in both dtypes).
+ */
+vtrace_status vtrace_gather_logits(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    void* gathered, vtrace_stream_t stream);
+
+/*
+ * Synchronises `stream`, then reads the workspace's sticky out-of-range-action
+ * flag into *flag (host pointer; 0 = no invalid action seen since the last
+ * vtrace_workspace_init).
+ */
+vtrace_status vtrace_error_flag(const void* workspace, int32_t* flag, vtrace_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VTRACE_H_ */

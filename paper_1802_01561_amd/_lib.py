@@ -1,0 +1,73 @@
+"""ctypes declarations of the libvtrace C ABI (include/vtrace.h).
+
+Loading fails loudly when the library has not been built: there is no
+fallback implementation anywhere in this package.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvtrace.so")
+
+VTRACE_F32 = 0
+VTRACE_BF16 = 1
+STATUS_NAMES = {
+    0: "VTRACE_OK",
+    1: "VTRACE_ERR_NULL",
+    2: "VTRACE_ERR_SHAPE",
+    3: "VTRACE_ERR_DTYPE",
+    4: "VTRACE_ERR_PARAM",
+    5: "VTRACE_ERR_ALIGN",
+    6: "VTRACE_ERR_WORKSPACE",
+    7: "VTRACE_ERR_HIP",
+}
+
+# Every symbol include/vtrace.h declares, with (restype, argtypes).
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_INPUTS = [_I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _F, _F, _F]
+SIGNATURES = {
+    "vtrace_abi_version": (ctypes.c_int, []),
+    "vtrace_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "vtrace_max_elements": (ctypes.c_int64, []),
+    "vtrace_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
+    "vtrace_workspace_init": (ctypes.c_int, [_P, ctypes.c_size_t, _P]),
+    "vtrace_targets": (ctypes.c_int, _INPUTS + [_P, _P, _P, ctypes.c_size_t, _P]),
+    "vtrace_loss_grad": (ctypes.c_int, _INPUTS + [_F, _F, _P, _P, _P, _P, _P, _P, _P,
+                                                  ctypes.c_size_t, _P]),
+    "vtrace_gather_logits": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _P, _P]),
+    "vtrace_error_flag": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), _P]),
+}
+
+_lib = None
+
+
+class VtraceError(RuntimeError):
+    def __init__(self, status: int, lib):
+        msg = lib.vtrace_status_string(status).decode()
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib():
+    """The loaded library, with argument types declared."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_1802_01561_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def check(status: int) -> None:
+    if status != 0:
+        raise VtraceError(status, lib())

@@ -1,0 +1,192 @@
+"""Torch-tensor front end of libvtrace: argument marshalling only.
+
+Every step of the computation runs in the HIP kernels behind the C ABI; torch
+only provides device memory and the current HIP stream.  Function names match
+the C entry points in include/vtrace.h.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from typing import NamedTuple, Optional
+
+import torch
+
+from ._lib import VTRACE_BF16, VTRACE_F32, check, lib
+
+__all__ = [
+    "LossGrad",
+    "Workspace",
+    "vtrace_abi_version",
+    "vtrace_error_flag",
+    "vtrace_gather_logits",
+    "vtrace_loss_grad",
+    "vtrace_max_elements",
+    "vtrace_targets",
+    "vtrace_workspace_bytes",
+]
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return VTRACE_F32
+    if t.dtype == torch.bfloat16:
+        return VTRACE_BF16
+    raise TypeError(f"logits must be float32 or bfloat16, got {t.dtype}")
+
+
+def _require(t: torch.Tensor, name: str, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values, bootstrap_value):
+    if target_logits.dim() != 3:
+        raise ValueError("target_logits must be [T, B, A]")
+    T, B, A = target_logits.shape
+    dev = target_logits.device
+    if dev.type != "cuda":
+        raise ValueError("inputs must be on a GPU device")
+    code = _dtype_code(target_logits)
+    _require(target_logits, "target_logits", (T, B, A), None, dev)
+    _require(behaviour_logits, "behaviour_logits", (T, B, A), target_logits.dtype, dev)
+    _require(actions, "actions", (T, B), torch.int32, dev)
+    for name, t in (("rewards", rewards), ("discounts", discounts), ("values", values)):
+        _require(t, name, (T, B), torch.float32, dev)
+    _require(bootstrap_value, "bootstrap_value", (B,), torch.float32, dev)
+    return T, B, A, code, dev
+
+
+def vtrace_abi_version() -> int:
+    return lib().vtrace_abi_version()
+
+
+def vtrace_max_elements() -> int:
+    return lib().vtrace_max_elements()
+
+
+def vtrace_workspace_bytes(T: int, B: int, A: int) -> int:
+    return lib().vtrace_workspace_bytes(T, B, A)
+
+
+class Workspace:
+    """Device workspace for vtrace_loss_grad, cleared on creation."""
+
+    def __init__(self, T: int, B: int, A: int, device=None, stream=None):
+        n = vtrace_workspace_bytes(T, B, A)
+        if n == 0:
+            raise ValueError(f"invalid batch shape T={T} B={B} A={A}")
+        self.nbytes = n
+        self.tensor = torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+        check(lib().vtrace_workspace_init(_p(self.tensor), n, _stream(stream)))
+
+    def fits(self, T: int, B: int, A: int) -> bool:
+        return self.nbytes >= vtrace_workspace_bytes(T, B, A)
+
+
+class LossGrad(NamedTuple):
+    losses: torch.Tensor  # [4] total, policy gradient, baseline, entropy
+    d_logits: torch.Tensor  # [T,B,A]
+    d_values: torch.Tensor  # [T,B]
+    vs: Optional[torch.Tensor]
+    pg_advantages: Optional[torch.Tensor]
+    lane_losses: Optional[torch.Tensor]
+
+
+def vtrace_targets(target_logits, behaviour_logits, actions, rewards, discounts, values,
+                   bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, vs=None,
+                   pg_advantages=None, workspace: Optional[Workspace] = None, stream=None):
+    """V-trace targets v_s and advantages; returns (vs, pg_advantages)."""
+    T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
+                                 values, bootstrap_value)
+    if vs is None:
+        vs = torch.empty((T, B), dtype=torch.float32, device=dev)
+    if pg_advantages is None:
+        pg_advantages = torch.empty((T, B), dtype=torch.float32, device=dev)
+    _require(vs, "vs", (T, B), torch.float32, dev)
+    _require(pg_advantages, "pg_advantages", (T, B), torch.float32, dev)
+    ws, nws = (None, 0) if workspace is None else (_p(workspace.tensor), workspace.nbytes)
+    check(lib().vtrace_targets(
+        T, B, A, code, _p(target_logits), _p(behaviour_logits), _p(actions), _p(rewards),
+        _p(discounts), _p(values), _p(bootstrap_value), rho_bar, c_bar, lam,
+        _p(vs), _p(pg_advantages), ws, nws, _stream(stream)))
+    return vs, pg_advantages
+
+
+def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discounts, values,
+                     bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, baseline_cost=0.5,
+                     entropy_cost=0.01, *, workspace: Optional[Workspace] = None,
+                     with_vs=False, with_pg_advantages=False, with_lane_losses=False,
+                     out: Optional[LossGrad] = None, stream=None) -> LossGrad:
+    """Fused V-trace targets, losses and gradients w.r.t. logits and values.
+
+    ``out`` may hold preallocated output tensors (fields left None are skipped
+    when optional, allocated when required)."""
+    T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
+                                 values, bootstrap_value)
+    if workspace is None:
+        workspace = Workspace(T, B, A, device=dev, stream=stream)
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        out = LossGrad(
+            torch.empty(4, **f32), torch.empty((T, B, A), **f32), torch.empty((T, B), **f32),
+            torch.empty((T, B), **f32) if with_vs else None,
+            torch.empty((T, B), **f32) if with_pg_advantages else None,
+            torch.empty((B, 3), **f32) if with_lane_losses else None)
+    _require(out.losses, "losses", (4,), torch.float32, dev)
+    _require(out.d_logits, "d_logits", (T, B, A), torch.float32, dev)
+    _require(out.d_values, "d_values", (T, B), torch.float32, dev)
+    if out.vs is not None:
+        _require(out.vs, "vs", (T, B), torch.float32, dev)
+    if out.pg_advantages is not None:
+        _require(out.pg_advantages, "pg_advantages", (T, B), torch.float32, dev)
+    if out.lane_losses is not None:
+        _require(out.lane_losses, "lane_losses", (B, 3), torch.float32, dev)
+    check(lib().vtrace_loss_grad(
+        T, B, A, code, _p(target_logits), _p(behaviour_logits), _p(actions), _p(rewards),
+        _p(discounts), _p(values), _p(bootstrap_value), rho_bar, c_bar, lam,
+        baseline_cost, entropy_cost, _p(out.losses), _p(out.d_logits), _p(out.d_values),
+        _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses),
+        _p(workspace.tensor), workspace.nbytes, _stream(stream)))
+    return out
+
+
+def vtrace_gather_logits(target_logits, behaviour_logits, actions, *, gathered=None, stream=None):
+    """[T,B,2] bit copies of the target and behaviour logits at the taken actions."""
+    if target_logits.dim() != 3:
+        raise ValueError("target_logits must be [T, B, A]")
+    T, B, A = target_logits.shape
+    dev = target_logits.device
+    code = _dtype_code(target_logits)
+    _require(behaviour_logits, "behaviour_logits", (T, B, A), target_logits.dtype, dev)
+    _require(actions, "actions", (T, B), torch.int32, dev)
+    if gathered is None:
+        gathered = torch.empty((T, B, 2), dtype=target_logits.dtype, device=dev)
+    _require(gathered, "gathered", (T, B, 2), target_logits.dtype, dev)
+    check(lib().vtrace_gather_logits(T, B, A, code, _p(target_logits), _p(behaviour_logits),
+                                     _p(actions), _p(gathered), _stream(stream)))
+    return gathered
+
+
+def vtrace_error_flag(workspace: Workspace, stream=None) -> int:
+    """Synchronises the stream and returns the sticky out-of-range-action flag."""
+    flag = ctypes.c_int32(0)
+    check(lib().vtrace_error_flag(_p(workspace.tensor), ctypes.byref(flag), _stream(stream)))
+    return int(flag.value)

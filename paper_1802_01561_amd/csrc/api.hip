@@ -1,0 +1,243 @@
+// C ABI of libvtrace: argument validation, kernel choice and launch.
+#include <cmath>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+
+#include "../../include/vtrace.h"
+#include "launch.hpp"
+
+namespace {
+
+using vtrace::LogitsType;
+using vtrace::Mode;
+using vtrace::StepArgs;
+
+constexpr int kAbiVersion = 1;
+constexpr int64_t kMaxElements = int64_t(1) << 40;
+
+bool shape_ok(int64_t T, int64_t B, int64_t A) {
+  if (T < 1 || B < 1 || A < 1) return false;
+  if (T > kMaxElements || B > kMaxElements || A > kMaxElements) return false;
+  const __int128 n = static_cast<__int128>(T) * B * A;
+  return n <= kMaxElements;
+}
+
+bool aligned(const void* p, uintptr_t k) { return (reinterpret_cast<uintptr_t>(p) % k) == 0; }
+
+bool truncation_ok(float x) { return !std::isnan(x) && x >= 0.0f; }
+
+hipStream_t as_hip(vtrace_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool dtype_of(vtrace_dtype d, LogitsType* lt) {
+  if (d == VTRACE_F32) {
+    *lt = LogitsType::F32;
+    return true;
+  }
+  if (d == VTRACE_BF16) {
+    *lt = LogitsType::BF16;
+    return true;
+  }
+  return false;
+}
+
+// Kernel choice: the tiled kernel where it applies, else the generic one.
+// VTRACE_KERNEL=lane_serial forces the generic kernel (used to cross-check the two).
+bool force_lane_serial() {
+  const char* k = std::getenv("VTRACE_KERNEL");
+  return k != nullptr && std::strcmp(k, "lane_serial") == 0;
+}
+
+size_t workspace_bytes_for(int64_t B) {
+  const int64_t max_wg = (B + vtrace::kMinLanesPerWorkgroup - 1) / vtrace::kMinLanesPerWorkgroup;
+  return vtrace::kWsHeaderBytes + 3 * sizeof(double) * static_cast<size_t>(max_wg);
+}
+
+vtrace_status check_common(int64_t T, int64_t B, int64_t A, vtrace_dtype dt, const void* tl,
+                           const void* bl, const int32_t* act, const float* r, const float* d,
+                           const float* v, const float* boot, float rho_bar, float c_bar,
+                           float lambda, LogitsType* lt) {
+  if (!tl || !bl || !act || !r || !d || !v || !boot) return VTRACE_ERR_NULL;
+  if (!shape_ok(T, B, A)) return VTRACE_ERR_SHAPE;
+  if (!dtype_of(dt, lt)) return VTRACE_ERR_DTYPE;
+  if (!truncation_ok(rho_bar) || !truncation_ok(c_bar)) return VTRACE_ERR_PARAM;
+  if (std::isnan(lambda) || lambda < 0.0f || lambda > 1.0f) return VTRACE_ERR_PARAM;
+  if (!aligned(tl, 16) || !aligned(bl, 16)) return VTRACE_ERR_ALIGN;
+  if (!aligned(act, 4) || !aligned(r, 4) || !aligned(d, 4) || !aligned(v, 4) || !aligned(boot, 4))
+    return VTRACE_ERR_ALIGN;
+  return VTRACE_OK;
+}
+
+StepArgs make_args(int64_t T, int64_t B, int64_t A, const void* tl, const void* bl,
+                   const int32_t* act, const float* r, const float* d, const float* v,
+                   const float* boot, float rho_bar, float c_bar, float lambda) {
+  StepArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.T = T;
+  a.B = B;
+  a.A = A;
+  a.target_logits = tl;
+  a.behaviour_logits = bl;
+  a.actions = act;
+  a.rewards = r;
+  a.discounts = d;
+  a.values = v;
+  a.bootstrap_value = boot;
+  a.rho_bar = rho_bar;
+  a.c_bar = c_bar;
+  a.lambda = lambda;
+  return a;
+}
+
+void attach_workspace(StepArgs* a, void* ws) {
+  char* base = static_cast<char*>(ws);
+  a->ticket = reinterpret_cast<unsigned int*>(base + vtrace::kWsTicketOffset);
+  a->error_flag = reinterpret_cast<unsigned int*>(base + vtrace::kWsFlagOffset);
+  a->partials = reinterpret_cast<double*>(base + vtrace::kWsHeaderBytes);
+}
+
+vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s) {
+  (void)hipGetLastError();  // do not report an earlier, unrelated error
+  int64_t nwg = 0;
+  hipError_t e;
+  if (!force_lane_serial() && vtrace::tiled_supported(a, lt))
+    e = vtrace::launch_tiled(a, lt, mode, s, &nwg);
+  else
+    e = vtrace::launch_lane_serial(a, lt, mode, s, &nwg);
+  return e == hipSuccess ? VTRACE_OK : VTRACE_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vtrace_abi_version(void) { return kAbiVersion; }
+
+const char* vtrace_status_string(vtrace_status s) {
+  switch (s) {
+    case VTRACE_OK: return "ok";
+    case VTRACE_ERR_NULL: return "a required pointer is NULL";
+    case VTRACE_ERR_SHAPE: return "T, B and A must be >= 1 and T*B*A within vtrace_max_elements()";
+    case VTRACE_ERR_DTYPE: return "unknown logits dtype";
+    case VTRACE_ERR_PARAM:
+      return "bad parameter: rho_bar, c_bar must be >= 0 (inf allowed), lambda in [0,1], "
+             "costs finite, none NaN";
+    case VTRACE_ERR_ALIGN: return "misaligned pointer: logits/d_logits/gathered need 16 bytes, others 4";
+    case VTRACE_ERR_WORKSPACE: return "workspace missing or smaller than vtrace_workspace_bytes()";
+    case VTRACE_ERR_HIP: return "the HIP runtime rejected the kernel launch";
+  }
+  return "unknown status";
+}
+
+int64_t vtrace_max_elements(void) { return kMaxElements; }
+
+size_t vtrace_workspace_bytes(int64_t T, int64_t B, int64_t A) {
+  if (!shape_ok(T, B, A)) return 0;
+  return workspace_bytes_for(B);
+}
+
+vtrace_status vtrace_workspace_init(void* workspace, size_t workspace_bytes, vtrace_stream_t stream) {
+  if (!workspace) return VTRACE_ERR_NULL;
+  if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
+  if (workspace_bytes < vtrace::kWsHeaderBytes) return VTRACE_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return vtrace::launch_fill_zero(workspace, workspace_bytes, as_hip(stream)) == hipSuccess
+             ? VTRACE_OK
+             : VTRACE_ERR_HIP;
+}
+
+vtrace_status vtrace_targets(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                             const void* target_logits, const void* behaviour_logits,
+                             const int32_t* actions, const float* rewards, const float* discounts,
+                             const float* values, const float* bootstrap_value, float rho_bar,
+                             float c_bar, float lambda, float* vs, float* pg_advantages,
+                             void* workspace, size_t workspace_bytes, vtrace_stream_t stream) {
+  LogitsType lt;
+  vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
+                                  rewards, discounts, values, bootstrap_value, rho_bar, c_bar,
+                                  lambda, &lt);
+  if (st != VTRACE_OK) return st;
+  if (!vs || !pg_advantages) return VTRACE_ERR_NULL;
+  if (!aligned(vs, 4) || !aligned(pg_advantages, 4)) return VTRACE_ERR_ALIGN;
+  StepArgs a = make_args(T, B, A, target_logits, behaviour_logits, actions, rewards, discounts,
+                         values, bootstrap_value, rho_bar, c_bar, lambda);
+  a.vs = vs;
+  a.pg_adv = pg_advantages;
+  if (workspace) {
+    if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
+    if (workspace_bytes < vtrace::kWsHeaderBytes) return VTRACE_ERR_WORKSPACE;
+    attach_workspace(&a, workspace);
+    a.partials = nullptr;
+    a.ticket = nullptr;
+  }
+  return launch(a, lt, Mode::Targets, as_hip(stream));
+}
+
+vtrace_status vtrace_loss_grad(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                               const void* target_logits, const void* behaviour_logits,
+                               const int32_t* actions, const float* rewards,
+                               const float* discounts, const float* values,
+                               const float* bootstrap_value, float rho_bar, float c_bar,
+                               float lambda, float baseline_cost, float entropy_cost,
+                               float* losses, float* d_logits, float* d_values, float* vs,
+                               float* pg_advantages, float* lane_losses, void* workspace,
+                               size_t workspace_bytes, vtrace_stream_t stream) {
+  LogitsType lt;
+  vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
+                                  rewards, discounts, values, bootstrap_value, rho_bar, c_bar,
+                                  lambda, &lt);
+  if (st != VTRACE_OK) return st;
+  if (!std::isfinite(baseline_cost) || !std::isfinite(entropy_cost)) return VTRACE_ERR_PARAM;
+  if (!losses || !d_logits || !d_values) return VTRACE_ERR_NULL;
+  if (!aligned(d_logits, 16)) return VTRACE_ERR_ALIGN;
+  if (!aligned(losses, 4) || !aligned(d_values, 4) || !aligned(vs, 4) ||
+      !aligned(pg_advantages, 4) || !aligned(lane_losses, 4))
+    return VTRACE_ERR_ALIGN;
+  if (!workspace) return VTRACE_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
+  if (workspace_bytes < workspace_bytes_for(B)) return VTRACE_ERR_WORKSPACE;
+  StepArgs a = make_args(T, B, A, target_logits, behaviour_logits, actions, rewards, discounts,
+                         values, bootstrap_value, rho_bar, c_bar, lambda);
+  a.baseline_cost = baseline_cost;
+  a.entropy_cost = entropy_cost;
+  a.losses = losses;
+  a.d_logits = d_logits;
+  a.d_values = d_values;
+  a.vs = vs;
+  a.pg_adv = pg_advantages;
+  a.lane_losses = lane_losses;
+  attach_workspace(&a, workspace);
+  return launch(a, lt, Mode::LossGrad, as_hip(stream));
+}
+
+vtrace_status vtrace_gather_logits(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                                   const void* target_logits, const void* behaviour_logits,
+                                   const int32_t* actions, void* gathered, vtrace_stream_t stream) {
+  if (!target_logits || !behaviour_logits || !actions || !gathered) return VTRACE_ERR_NULL;
+  if (!shape_ok(T, B, A)) return VTRACE_ERR_SHAPE;
+  LogitsType lt;
+  if (!dtype_of(logits_dtype, &lt)) return VTRACE_ERR_DTYPE;
+  if (!aligned(target_logits, 16) || !aligned(behaviour_logits, 16) || !aligned(gathered, 16))
+    return VTRACE_ERR_ALIGN;
+  if (!aligned(actions, 4)) return VTRACE_ERR_ALIGN;
+  (void)hipGetLastError();
+  return vtrace::launch_gather(T, B, A, lt, target_logits, behaviour_logits, actions, gathered,
+                               as_hip(stream)) == hipSuccess
+             ? VTRACE_OK
+             : VTRACE_ERR_HIP;
+}
+
+vtrace_status vtrace_error_flag(const void* workspace, int32_t* flag, vtrace_stream_t stream) {
+  if (!workspace || !flag) return VTRACE_ERR_NULL;
+  if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
+  uint32_t v = 0;
+  hipStream_t s = as_hip(stream);
+  if (hipMemcpyAsync(&v, static_cast<const char*>(workspace) + vtrace::kWsFlagOffset, sizeof(v),
+                     hipMemcpyDeviceToHost, s) != hipSuccess)
+    return VTRACE_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return VTRACE_ERR_HIP;
+  *flag = static_cast<int32_t>(v);
+  return VTRACE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,114 @@
+// Device helpers shared by the V-trace kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "launch.hpp"
+
+namespace vtrace {
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float logit_to_float(float x) { return x; }
+__device__ __forceinline__ float logit_to_float(uint16_t bits) {
+  return __uint_as_float(static_cast<uint32_t>(bits) << 16);
+}
+
+// min(bar, x) as in the truncated weights of Sec. 4.1, written so that a NaN
+// ratio stays NaN (fmin would return `bar`).  min(+inf, x) = x.
+__device__ __forceinline__ double clip_above(double x, double bar) { return x > bar ? bar : x; }
+
+// pi(a|x)/mu(a|x) from the max-shifted logits at the taken action and the two
+// exponent sums s = sum_j exp(l_j - max_j l_j):
+//   ratio = exp((z_a - m_z) - (y_a - m_y)) * s_mu / s_pi.
+// The differences of two floats are exact in float64, so the only float32
+// rounding left is in the exponentials that make up the sums.
+__device__ __forceinline__ double importance_ratio(float za, float mz, float ya, float my,
+                                                   double s_pi, double s_mu) {
+  const double dz = static_cast<double>(za) - static_cast<double>(mz);
+  const double dy = static_cast<double>(ya) - static_cast<double>(my);
+  return exp(dz - dy) * (s_mu / s_pi);
+}
+
+// Butterfly sum over a wave.  Every lane ends with the same value, and the
+// order of additions is fixed, so the result is reproducible bit for bit.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+// Sum of three per-thread values over the block, in a fixed order.  The result
+// is valid in thread 0.  `scratch` holds 3 doubles per wave.
+template <int kThreads>
+__device__ __forceinline__ void block_sum3(double& x0, double& x1, double& x2, double* scratch) {
+  x0 = wave_sum(x0);
+  x1 = wave_sum(x1);
+  x2 = wave_sum(x2);
+  if constexpr (kThreads > kWave) {
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x % kWave) == 0) {
+      scratch[3 * w + 0] = x0;
+      scratch[3 * w + 1] = x1;
+      scratch[3 * w + 2] = x2;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      x0 = scratch[0];
+      x1 = scratch[1];
+      x2 = scratch[2];
+      for (int i = 1; i < kThreads / kWave; ++i) {
+        x0 += scratch[3 * i + 0];
+        x1 += scratch[3 * i + 1];
+        x2 += scratch[3 * i + 2];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Cross-workgroup loss reduction in the same launch.  Each workgroup stores its
+// three partial sums, then takes a ticket; the workgroup that draws the last
+// ticket adds all partials in workgroup order, writes `losses` and rearms the
+// counter for the next call.  Every thread of every workgroup must call this.
+template <int kThreads>
+__device__ void finish_losses(const StepArgs& a, double pg, double base, double ent,
+                              double* scratch) {
+  __shared__ int s_last;
+  block_sum3<kThreads>(pg, base, ent, scratch);
+  if (threadIdx.x == 0) {
+    double* p = a.partials + 3 * static_cast<size_t>(blockIdx.x);
+    p[0] = pg;
+    p[1] = base;
+    p[2] = ent;
+    __threadfence();  // release the partials before the ticket
+    const unsigned prev = atomicAdd(a.ticket, 1u);
+    s_last = (prev == gridDim.x - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();  // acquire: every other workgroup's partials are visible
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+  for (unsigned i = threadIdx.x; i < gridDim.x; i += kThreads) {
+    const double* p = a.partials + 3 * static_cast<size_t>(i);
+    s0 += __hip_atomic_load(p + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s1 += __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s2 += __hip_atomic_load(p + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  block_sum3<kThreads>(s0, s1, s2, scratch);
+  if (threadIdx.x == 0) {
+    a.losses[0] = static_cast<float>(s0 + s1 + s2);
+    a.losses[1] = static_cast<float>(s0);
+    a.losses[2] = static_cast<float>(s1);
+    a.losses[3] = static_cast<float>(s2);
+    __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+__device__ __forceinline__ void raise_error_flag(unsigned int* flag) {
+  if (flag != nullptr) atomicOr(flag, 1u);
+}
+
+}  // namespace vtrace

@@ -1,0 +1,138 @@
+// Generic V-trace kernel: one thread per lane, walking time backwards.
+//
+// This is the any-A path (and the reference point for the tiled kernel).  Each
+// thread owns lane b and visits t = T-1 .. 0, so the reverse recursion of
+// Remark 1 is a plain loop and v_{t+1} is already known when step t needs it
+// for its advantage: the whole step (log-softmaxes, ratio, delta, recursion,
+// advantage, gradients, loss partials) is one pass over the lane's data.  Rows
+// are read straight from global memory; that is simple but not coalesced, which
+// is why the common action counts use the tiled kernel instead.
+#include "device_common.hpp"
+
+namespace vtrace {
+namespace {
+
+constexpr int kLaneSerialThreads = 64;
+
+template <typename In, bool kGrad>
+__global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArgs a) {
+  __shared__ double red_scratch[3 * (kLaneSerialThreads / kWave)];
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * kLaneSerialThreads + threadIdx.x;
+  const int64_t T = a.T, B = a.B, A = a.A;
+  const In* __restrict__ zlog = static_cast<const In*>(a.target_logits);
+  const In* __restrict__ ylog = static_cast<const In*>(a.behaviour_logits);
+  const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
+  const float ce = a.entropy_cost;
+
+  double acc_pg = 0.0, acc_base = 0.0, acc_ent = 0.0;
+  if (b < B) {
+    // Carries from step t+1: V(x_{t+1}), v_{t+1} and v_{t+1} - V(x_{t+1}).
+    const double boot = a.bootstrap_value[b];
+    double V_next = boot, v_next = boot, A_next = 0.0;
+    for (int64_t t = T - 1; t >= 0; --t) {
+      const int64_t idx = t * B + b;
+      const In* zr = zlog + idx * A;
+      const In* yr = ylog + idx * A;
+      const int32_t act = a.actions[idx];
+      const bool valid = act >= 0 && act < A;
+
+      // Row maxima and the logits at the taken action.
+      float mz = -INFINITY, my = -INFINITY, za = 0.f, ya = 0.f;
+      for (int64_t j = 0; j < A; ++j) {
+        const float z = logit_to_float(zr[j]);
+        const float y = logit_to_float(yr[j]);
+        mz = fmaxf(mz, z);
+        my = fmaxf(my, y);
+        if (j == act) {
+          za = z;
+          ya = y;
+        }
+      }
+      // Exponent sums; also sum_j e_j (z_j - m_z), which gives the entropy as
+      // H = log s - (sum_j e_j (z_j - m_z)) / s.
+      double sz = 0.0, sy = 0.0;
+      float ea = 0.f, ed = 0.f;
+      for (int64_t j = 0; j < A; ++j) {
+        const float dz = logit_to_float(zr[j]) - mz;
+        const float e = expf(dz);
+        sz += e;
+        ed += e * dz;
+        if (j == act) ea = e;
+        sy += expf(logit_to_float(yr[j]) - my);
+      }
+
+      const double ratio = valid ? importance_ratio(za, mz, ya, my, sz, sy) : NAN;
+      if (!valid) raise_error_flag(a.error_flag);
+      const double rho = clip_above(ratio, rho_bar);
+      const double c = lam * clip_above(ratio, c_bar);
+
+      const double r = a.rewards[idx], g = a.discounts[idx], V = a.values[idx];
+      const double delta = rho * (r + g * V_next - V);
+      const double A_t = delta + g * c * A_next;  // v_t - V(x_t)
+      const double v_t = V + A_t;
+      const double adv = rho * (r + g * v_next - V);
+
+      if (a.vs) a.vs[idx] = static_cast<float>(v_t);
+      if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+
+      if constexpr (kGrad) {
+        a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+        const float szf = static_cast<float>(sz);
+        const float inv = 1.0f / szf;
+        const float log_s = logf(szf);
+        const float H = log_s - ed * inv;
+        // 1 - pi(a): the other actions' mass, without cancellation.
+        const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) / sz);
+        const float adv32 = valid ? static_cast<float>(adv) : NAN;
+        float* dl = a.d_logits + idx * A;
+        for (int64_t j = 0; j < A; ++j) {
+          const float dz = logit_to_float(zr[j]) - mz;
+          const float p = expf(dz) * inv;
+          const float pg_term = (j == act) ? -one_minus_pa : p;
+          dl[j] = adv32 * pg_term + ce * p * ((dz - log_s) + H);
+        }
+        const double log_pa = valid ? static_cast<double>(za - mz) - static_cast<double>(log_s) : NAN;
+        acc_pg += -adv * log_pa;
+        acc_base += 0.5 * (v_t - V) * (v_t - V);
+        acc_ent += -static_cast<double>(H);
+      }
+      V_next = V;
+      v_next = v_t;
+      A_next = A_t;
+    }
+    if constexpr (kGrad) {
+      acc_base *= a.baseline_cost;
+      acc_ent *= a.entropy_cost;
+      if (a.lane_losses) {
+        a.lane_losses[3 * b + 0] = static_cast<float>(acc_pg);
+        a.lane_losses[3 * b + 1] = static_cast<float>(acc_base);
+        a.lane_losses[3 * b + 2] = static_cast<float>(acc_ent);
+      }
+    }
+  }
+  if constexpr (kGrad) finish_losses<kLaneSerialThreads>(a, acc_pg, acc_base, acc_ent, red_scratch);
+}
+
+template <typename In>
+hipError_t launch_typed(const StepArgs& a, Mode mode, hipStream_t s, int64_t* nwg) {
+  const int64_t blocks = (a.B + kLaneSerialThreads - 1) / kLaneSerialThreads;
+  *nwg = blocks;
+  if (mode == Mode::LossGrad) {
+    hipLaunchKernelGGL((lane_serial_kernel<In, true>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kLaneSerialThreads), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((lane_serial_kernel<In, false>), dim3(static_cast<unsigned>(blocks)),
+                       dim3(kLaneSerialThreads), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_lane_serial(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                              int64_t* num_workgroups) {
+  if (lt == LogitsType::BF16) return launch_typed<uint16_t>(a, mode, s, num_workgroups);
+  return launch_typed<float>(a, mode, s, num_workgroups);
+}
+
+}  // namespace vtrace

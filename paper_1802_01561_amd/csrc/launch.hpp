@@ -1,0 +1,59 @@
+// Host-side declarations shared by the C ABI and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace vtrace {
+
+// Everything one V-trace launch needs, passed by value to the kernels.
+struct StepArgs {
+  int64_t T, B, A;
+  const void* target_logits;     // [T,B,A] f32 or bf16
+  const void* behaviour_logits;  // [T,B,A]
+  const int32_t* actions;        // [T,B]
+  const float* rewards;          // [T,B]
+  const float* discounts;        // [T,B]
+  const float* values;           // [T,B]
+  const float* bootstrap_value;  // [B]
+  float rho_bar, c_bar, lambda;
+  float baseline_cost, entropy_cost;
+  // outputs (any may be null except where a kernel variant requires them)
+  float* losses;       // [4]
+  float* d_logits;     // [T,B,A]
+  float* d_values;     // [T,B]
+  float* vs;           // [T,B]
+  float* pg_adv;       // [T,B]
+  float* lane_losses;  // [B,3]
+  // workspace pieces (null when no workspace was given)
+  unsigned int* ticket;
+  unsigned int* error_flag;
+  double* partials;  // [num_workgroups, 3]
+};
+
+// Workspace layout: a 256-byte header (completion counter, error flag) and then
+// three float64 partial sums per workgroup.
+constexpr size_t kWsHeaderBytes = 256;
+constexpr size_t kWsTicketOffset = 0;
+constexpr size_t kWsFlagOffset = 4;
+// Every loss kernel covers at least this many lanes per workgroup, so the
+// partials array is sized by ceil(B / kMinLanesPerWorkgroup).
+constexpr int64_t kMinLanesPerWorkgroup = 4;
+
+enum class LogitsType { F32, BF16 };
+enum class Mode { Targets, LossGrad };
+
+// Kernel launchers.  They return the HIP status of the launch.
+hipError_t launch_lane_serial(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                              int64_t* num_workgroups);
+bool tiled_supported(const StepArgs& a, LogitsType lt);
+hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                        int64_t* num_workgroups);
+hipError_t launch_gather(int64_t T, int64_t B, int64_t A, LogitsType lt, const void* target,
+                         const void* behaviour, const int32_t* actions, void* gathered,
+                         hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+
+}  // namespace vtrace

@@ -1,0 +1,154 @@
+"""The C ABI on the host: exported symbols and argument validation.
+
+Every call here carries at least one invalid argument, so the library returns
+its status before any device work; nothing is launched.  (Fake pointers are
+only ever paired with an argument that fails validation.)
+"""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_1802_01561_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vtrace.h")
+
+OK, NULL, SHAPE, DTYPE, PARAM, ALIGN, WS = 0, 1, 2, 3, 4, 5, 6
+P = 0x10000  # a 16-byte-aligned fake device address, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L():
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(vtrace_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) == 9
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_version_and_strings(L):
+    assert L.vtrace_abi_version() == 1
+    for s in range(8):
+        assert len(L.vtrace_status_string(s)) > 0
+    assert L.vtrace_status_string(99) == b"unknown status"
+    assert L.vtrace_max_elements() == 1 << 40
+
+
+def test_workspace_bytes(L):
+    assert L.vtrace_workspace_bytes(0, 4, 9) == 0
+    assert L.vtrace_workspace_bytes(5, -1, 9) == 0
+    assert L.vtrace_workspace_bytes(1 << 20, 1 << 20, 2) == 0
+    n1 = L.vtrace_workspace_bytes(5, 4, 9)
+    n2 = L.vtrace_workspace_bytes(5, 4096, 9)
+    assert 256 <= n1 < n2
+    assert L.vtrace_workspace_bytes(1000, 16384, 18) == L.vtrace_workspace_bytes(1, 16384, 1)
+
+
+def _targets(L, **kw):
+    a = dict(T=5, B=4, A=9, dt=0, tl=P, bl=P, act=P, r=P, d=P, v=P, boot=P, rho=1.0, c=1.0,
+             lam=1.0, vs=P, pg=P, ws=None, nws=0)
+    a.update(kw)
+    return L.vtrace_targets(a["T"], a["B"], a["A"], a["dt"], a["tl"], a["bl"], a["act"], a["r"],
+                            a["d"], a["v"], a["boot"], a["rho"], a["c"], a["lam"], a["vs"], a["pg"],
+                            a["ws"], a["nws"], None)
+
+
+def _loss(L, **kw):
+    a = dict(T=5, B=4, A=9, dt=0, tl=P, bl=P, act=P, r=P, d=P, v=P, boot=P, rho=1.0, c=1.0,
+             lam=1.0, cv=0.5, ce=0.01, losses=P, dl=P, dv=P, vs=None, pg=None, lane=None,
+             ws=P, nws=1 << 20)
+    a.update(kw)
+    return L.vtrace_loss_grad(a["T"], a["B"], a["A"], a["dt"], a["tl"], a["bl"], a["act"], a["r"],
+                              a["d"], a["v"], a["boot"], a["rho"], a["c"], a["lam"], a["cv"],
+                              a["ce"], a["losses"], a["dl"], a["dv"], a["vs"], a["pg"], a["lane"],
+                              a["ws"], a["nws"], None)
+
+
+INVALID = [
+    # (kwargs, expected status) -- each case is rejected before any launch
+    (dict(tl=None), NULL), (dict(bl=None), NULL), (dict(act=None), NULL), (dict(r=None), NULL),
+    (dict(d=None), NULL), (dict(v=None), NULL), (dict(boot=None), NULL),
+    (dict(T=0), SHAPE), (dict(B=0), SHAPE), (dict(A=0), SHAPE), (dict(T=-3), SHAPE),
+    (dict(T=1 << 21, B=1 << 20), SHAPE),
+    (dict(dt=2), DTYPE), (dict(dt=-1), DTYPE),
+    (dict(rho=math.nan), PARAM), (dict(c=math.nan), PARAM), (dict(rho=-1.0), PARAM),
+    (dict(c=-0.5), PARAM), (dict(lam=1.5), PARAM), (dict(lam=-0.1), PARAM),
+    (dict(lam=math.nan), PARAM),
+    (dict(tl=P + 4), ALIGN), (dict(bl=P + 8), ALIGN), (dict(act=P + 2), ALIGN),
+    (dict(r=P + 1), ALIGN),
+]
+
+
+@pytest.mark.parametrize("kw,status", INVALID)
+def test_targets_rejects(L, kw, status):
+    assert _targets(L, **kw) == status
+
+
+def test_targets_rejects_outputs(L):
+    assert _targets(L, vs=None) == NULL
+    assert _targets(L, pg=None) == NULL
+    assert _targets(L, vs=P + 2) == ALIGN
+    assert _targets(L, ws=P + 4, nws=4096, rho=math.nan) == PARAM
+    assert _targets(L, ws=P + 4, nws=4096) == ALIGN
+    assert _targets(L, ws=P, nws=16) == WS
+
+
+@pytest.mark.parametrize("kw,status", INVALID)
+def test_loss_grad_rejects(L, kw, status):
+    assert _loss(L, **kw) == status
+
+
+def test_loss_grad_rejects_outputs_and_workspace(L):
+    assert _loss(L, losses=None) == NULL
+    assert _loss(L, dl=None) == NULL
+    assert _loss(L, dv=None) == NULL
+    assert _loss(L, dl=P + 4) == ALIGN
+    assert _loss(L, vs=P + 2) == ALIGN
+    assert _loss(L, lane=P + 1) == ALIGN
+    assert _loss(L, cv=math.inf) == PARAM
+    assert _loss(L, ce=math.nan) == PARAM
+    assert _loss(L, ws=None) == WS
+    assert _loss(L, nws=16) == WS
+    assert _loss(L, B=4096, nws=L.vtrace_workspace_bytes(5, 4096, 9) - 1) == WS
+    assert _loss(L, ws=P + 8) == ALIGN
+
+
+def test_gather_and_flag_reject(L):
+    g = L.vtrace_gather_logits
+    assert g(5, 4, 9, 0, None, P, P, P, None) == NULL
+    assert g(5, 4, 9, 0, P, P, P, None, None) == NULL
+    assert g(0, 4, 9, 0, P, P, P, P, None) == SHAPE
+    assert g(5, 4, 9, 7, P, P, P, P, None) == DTYPE
+    assert g(5, 4, 9, 0, P, P, P, P + 4, None) == ALIGN
+    flag = ctypes.c_int32(0)
+    assert L.vtrace_error_flag(None, ctypes.byref(flag), None) == NULL
+    assert L.vtrace_error_flag(P, None, None) == NULL
+    assert L.vtrace_error_flag(P + 4, ctypes.byref(flag), None) == ALIGN
+    assert L.vtrace_workspace_init(None, 1024, None) == NULL
+    assert L.vtrace_workspace_init(P + 4, 1024, None) == ALIGN
+    assert L.vtrace_workspace_init(P, 100, None) == WS
+
+
+def test_python_binding_validates_before_calling():
+    torch = pytest.importorskip("torch")
+    import paper_1802_01561_amd as v
+    z = torch.zeros(2, 3, 4)
+    with pytest.raises(ValueError):
+        v.vtrace_targets(z, z, torch.zeros(2, 3, dtype=torch.int32), torch.zeros(2, 3),
+                         torch.zeros(2, 3), torch.zeros(2, 3), torch.zeros(3))
+    with pytest.raises(TypeError):
+        v.binding._dtype_code(torch.zeros(1, dtype=torch.float16))

@@ -1,0 +1,268 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+fp32 outputs must satisfy |g - o| <= 1e-5 + 1e-4 |o| element by element;
+gathers must be bit-exact.  The oracle sees the same seeded inputs.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1802_01561_amd as vt
+from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from synth import PARAM_SETS, make_config, make_random, subset_lanes
+from synth.trajectories import STRESS_SUBSET
+
+pytestmark = pytest.mark.gpu
+
+
+def run_loss_grad(dev, p, **kw):
+    out = vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                              baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
+                              with_vs=True, with_pg_advantages=True, with_lane_losses=True, **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def check_against_oracle(tr, p, out, lanes=None):
+    """Compare every output of a loss_grad call with the oracle (optionally on a
+    subset of lanes, where the oracle runs on those lanes alone)."""
+    sub = tr if lanes is None else subset_lanes(tr, lanes)
+    o = oracle.loss_and_grads(*oracle_args(sub), p.rho_bar, p.c_bar, p.lam,
+                              p.baseline_cost, p.entropy_cost)
+    pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
+    assert_close("vs", pick(np_out(out.vs)), o.vs)
+    assert_close("pg_advantages", pick(np_out(out.pg_advantages)), o.pg_advantages)
+    assert_close("d_values", pick(np_out(out.d_values)), o.d_values)
+    assert_close("d_logits", pick(np_out(out.d_logits)), o.d_logits)
+    lane = np_out(out.lane_losses)
+    assert_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses)
+    if lanes is None:
+        assert_close("losses", np_out(out.losses), o.losses)
+    return o
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+@pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
+                                      (0, True), (2, True)])
+def test_config_matches_oracle(cfg, bf16):
+    tr = make_config(cfg, bf16=bf16)
+    for p in PARAM_SETS[cfg]:
+        log_case(f"config {cfg} ({tr.name}) {p.label()} T={tr.T} B={tr.B} A={tr.A}")
+        dev = to_device(tr)
+        out = run_loss_grad(dev, p)
+        check_against_oracle(tr, p, out)
+        vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
+        torch.cuda.synchronize()
+        o = oracle.vtrace(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam)
+        assert_close("targets.vs", np_out(vs), o.vs)
+        assert_close("targets.pg_advantages", np_out(pg), o.pg_advantages)
+        g = vt.vtrace_gather_logits(dev["target_logits"], dev["behaviour_logits"], dev["actions"])
+        torch.cuda.synchronize()
+        zt, yt = tr.logits_for_device()
+        expect = oracle.gather_action_logits(zt, yt, tr.actions)
+        got = g.cpu().view(torch.int16).numpy() if bf16 else g.cpu().numpy()
+        assert got.tobytes() == np.ascontiguousarray(expect).tobytes()
+
+
+@pytest.fixture(scope="module")
+def stress():
+    log_case("generating the stress batch T=1000 B=16384 A=18")
+    tr = make_config(4)
+    dev = to_device(tr)
+    return tr, dev
+
+
+@pytest.mark.parametrize("pidx", [0, 1, 2])
+def test_stress_subset_matches_oracle(stress, pidx):
+    tr, dev = stress
+    p = PARAM_SETS[4][pidx]
+    log_case(f"stress T=1000 B=16384 A=18 {p.label()}: full launch, oracle on 64 lanes")
+    out = run_loss_grad(dev, p)
+    check_against_oracle(tr, p, out, lanes=STRESS_SUBSET)
+    # the totals are the fixed-order sums of the per-lane partials
+    lane = np_out(out.lane_losses).astype(np.float64)
+    losses = np_out(out.losses).astype(np.float64)
+    assert_close("losses vs lane sums", losses[1:], lane.sum(axis=0), rtol=1e-4, atol=1e-3)
+    assert losses[0] == pytest.approx(losses[1:].sum(), rel=1e-6)
+
+
+EDGE_SHAPES = [
+    (1, 1, 1), (1, 5, 9), (2, 1, 18), (15, 3, 9), (16, 16, 18), (17, 17, 18), (33, 15, 9),
+    (31, 33, 9), (7, 64, 9), (5, 65, 18), (40, 31, 2), (9, 7, 3), (12, 10, 7), (20, 9, 17),
+    (11, 6, 33), (3, 4, 100), (65, 2, 5), (8, 129, 18), (24, 40, 9),
+]
+
+
+@pytest.mark.parametrize("T,B,A", EDGE_SHAPES)
+def test_edge_shapes(T, B, A):
+    tr = make_random(T, B, A, 1000 + T * 7 + B * 3 + A, noise_std=1.0, end_prob=0.05)
+    for p in (PARAM_SETS[4][1], PARAM_SETS[4][2]):
+        log_case(f"edge T={T} B={B} A={A} {p.label()}")
+        out = run_loss_grad(to_device(tr), p)
+        check_against_oracle(tr, p, out)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_edge_shapes_bf16(bf16):
+    for (T, B, A) in [(17, 65, 9), (5, 3, 18), (33, 130, 9)]:
+        tr = make_random(T, B, A, 77 + T, noise_std=1.0, bf16=bf16)
+        p = PARAM_SETS[4][0]
+        log_case(f"edge bf16={bf16} T={T} B={B} A={A}")
+        check_against_oracle(tr, p, run_loss_grad(to_device(tr), p))
+
+
+@pytest.mark.parametrize("case", ["extreme_logits", "all_ends", "lambda0", "no_clip", "cbar0",
+                                  "action0", "actionlast", "on_policy"])
+def test_degenerate_cases(case):
+    T, B, A = 37, 40, 18
+    kw = dict(noise_std=1.0)
+    if case == "extreme_logits":
+        kw["logit_scale"] = 80.0
+    tr = make_random(T, B, A, 4242, **kw)
+    p = PARAM_SETS[4][0]
+    if case == "all_ends":
+        tr.discounts[:] = 0.0
+    if case == "lambda0":
+        p = type(p)(1.0, 1.0, 0.0)
+    if case == "no_clip":
+        p = type(p)(math.inf, math.inf, 1.0)
+    if case == "cbar0":
+        p = type(p)(2.0, 0.0, 1.0)
+    if case == "action0":
+        tr.actions[:] = 0
+    if case == "actionlast":
+        tr.actions[:] = A - 1
+    if case == "on_policy":
+        tr.behaviour_logits = tr.target_logits.copy()
+    log_case(f"degenerate {case}")
+    out = run_loss_grad(to_device(tr), p)
+    check_against_oracle(tr, p, out)
+    if case == "all_ends":
+        pg = np_out(out.pg_advantages)
+        assert np.all(np.isfinite(pg))
+
+
+def test_out_of_range_actions_give_nan_and_flag():
+    tr = make_random(12, 10, 9, 5)
+    tr.actions[5, 3] = 9
+    tr.actions[2, 7] = -1
+    dev = to_device(tr)
+    ws = vt.Workspace(12, 10, 9)
+    log_case("out-of-range actions")
+    assert vt.vtrace_error_flag(ws) == 0
+    out = vt.vtrace_loss_grad(**dev, workspace=ws, with_vs=True, with_pg_advantages=True)
+    torch.cuda.synchronize()
+    assert vt.vtrace_error_flag(ws) == 1
+    dl = np_out(out.d_logits)
+    assert np.all(np.isnan(dl[5, 3])) and np.all(np.isnan(dl[2, 7]))
+    vs = np_out(out.vs)
+    assert np.isnan(vs[5, 3]) and np.all(np.isnan(vs[:5, 3]))
+    assert np.all(np.isfinite(vs[6:, 3]))  # later steps are untouched
+    good = [b for b in range(10) if b not in (3, 7)]
+    assert np.all(np.isfinite(vs[:, good]))
+    losses = np_out(out.losses)
+    assert np.isnan(losses[:3]).all() and np.isfinite(losses[3])  # entropy ignores actions
+    g = vt.vtrace_gather_logits(dev["target_logits"], dev["behaviour_logits"], dev["actions"])
+    gb = g.cpu().numpy().view(np.uint32)
+    assert gb[5, 3, 0] == 0xFFFFFFFF and gb[2, 7, 1] == 0xFFFFFFFF
+    # a cleared workspace starts without the flag; valid data does not raise it
+    ws2 = vt.Workspace(12, 10, 9)
+    tr.actions[5, 3] = 0
+    tr.actions[2, 7] = 0
+    vt.vtrace_loss_grad(**to_device(tr), workspace=ws2)
+    assert vt.vtrace_error_flag(ws2) == 0
+
+
+def test_deterministic_and_workspace_reuse():
+    tr = make_config(3)
+    dev = to_device(tr)
+    ws = vt.Workspace(tr.T, tr.B, tr.A)
+    p = PARAM_SETS[3][0]
+    log_case("determinism, config 3")
+    a = run_loss_grad(dev, p, workspace=ws)
+    b = run_loss_grad(dev, p, workspace=ws)
+    for x, y in zip(a, b):
+        assert np_out(x).tobytes() == np_out(y).tobytes()
+
+
+def test_lane_permutation_is_bit_exact():
+    tr = make_random(50, 96, 9, 8)
+    perm = np.random.default_rng(0).permutation(96)
+    p = PARAM_SETS[4][1]
+    log_case("lane permutation")
+    a = run_loss_grad(to_device(tr), p)
+    b = run_loss_grad(to_device(subset_lanes(tr, perm)), p)
+    for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+        x, y = np_out(getattr(a, name)), np_out(getattr(b, name))
+        assert x[:, perm].tobytes() == y.tobytes(), name
+    assert np_out(a.lane_losses)[perm].tobytes() == np_out(b.lane_losses).tobytes()
+
+
+def test_episode_cut_is_bit_exact():
+    T, B, A = 40, 33, 18
+    tr = make_random(T, B, A, 21, end_prob=0.0)
+    tcut = 17
+    tr.discounts[tcut] = 0.0
+    p = PARAM_SETS[4][1]
+    log_case("episode cut")
+    a = run_loss_grad(to_device(tr), p)
+    other = make_random(T, B, A, 22)
+    for name in ("target_logits", "behaviour_logits", "actions", "rewards", "discounts", "values"):
+        arr = getattr(tr, name).copy()
+        arr[tcut + 1:] = getattr(other, name)[tcut + 1:]
+        setattr(tr, name, arr)
+    tr.bootstrap_value = other.bootstrap_value
+    b = run_loss_grad(to_device(tr), p)
+    for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+        x, y = np_out(getattr(a, name)), np_out(getattr(b, name))
+        assert x[:tcut + 1].tobytes() == y[:tcut + 1].tobytes(), name
+
+
+def test_gradient_invariants():
+    tr = make_random(30, 50, 18, 9, noise_std=1.0)
+    dev = to_device(tr)
+    p = type(PARAM_SETS[4][0])(1.0, 1.0, 1.0, 0.5, 0.0)
+    log_case("gradient invariants (entropy cost 0)")
+    out = run_loss_grad(dev, p)
+    dl = np_out(out.d_logits).astype(np.float64)
+    adv = np_out(out.pg_advantages).astype(np.float64)
+    np.testing.assert_allclose(dl.sum(-1), 0.0, atol=1e-5 + 1e-5 * np.abs(adv).max())
+    taken = np.take_along_axis(dl, tr.actions[..., None].astype(np.int64), -1)[..., 0]
+    nz = adv != 0
+    assert np.all(np.sign(taken[nz]) == -np.sign(adv[nz]))
+    # shifting each row of target logits by a constant leaves everything unchanged
+    shifted = tr.target_logits + np.float32(3.0)
+    tr2 = make_random(30, 50, 18, 9, noise_std=1.0)
+    tr2.target_logits = shifted
+    tr2.behaviour_logits = tr.behaviour_logits + np.float32(-2.0)
+    out2 = run_loss_grad(to_device(tr2), p)
+    for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+        assert_close(f"shift {name}", np_out(getattr(out2, name)), np_out(getattr(out, name)))
+    # a single action: no policy gradient
+    tr1 = make_random(10, 8, 1, 10)
+    out1 = run_loss_grad(to_device(tr1), PARAM_SETS[0][0])
+    assert np.all(np_out(out1.d_logits) == 0.0)
+
+
+def test_kernels_agree(monkeypatch):
+    """The tiled kernel and the generic lane-serial kernel give the same results."""
+    for (T, B, A, bf16) in [(100, 4096, 9, False), (60, 1000, 18, False), (50, 777, 9, True)]:
+        tr = make_random(T, B, A, 31 + A, noise_std=1.0, bf16=bf16)
+        dev = to_device(tr)
+        p = PARAM_SETS[4][1]
+        log_case(f"kernel agreement T={T} B={B} A={A} bf16={bf16}")
+        a = run_loss_grad(dev, p)
+        monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
+        b = run_loss_grad(dev, p)
+        monkeypatch.delenv("VTRACE_KERNEL")
+        for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses", "losses"):
+            assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
+                         np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
