@@ -4,24 +4,28 @@
 // Work split.  A workgroup owns LANES consecutive lanes (batch entries) for the
 // whole unroll and walks time backwards in chunks of L = 16 steps, so every
 // carry of the reverse recursion stays inside the workgroup.  Within a chunk,
-// thread (lane, s) handles step t = t0 + s; the 16 threads of one lane form one
-// row of a wave.
+// thread (lane, s) handles step t = t0 + s; the 16 threads of one lane are one
+// DPP row of a wave.
 //
 // Data path per chunk.
-//  1. The chunk's [L, LANES, A] slabs of target and behaviour logits are, for
-//     each t, one contiguous run of LANES*A elements (1152 bytes for every
-//     supported shape, nine 128-byte lines).  Threads copy them with 16-byte
-//     loads into LDS.  The copy of chunk k+1 is issued before chunk k is
-//     computed, so its latency hides behind the arithmetic.
-//  2. Each thread reads its own two rows from LDS: max, exponent sums, the
-//     importance ratio (float64, see device_common.hpp), rho and c.
+//  1. For each t the chunk's logits are one contiguous run of LANES*A elements
+//     (1152 bytes for every supported shape: nine 128-byte lines).  Threads copy
+//     both tensors' runs with 16-byte loads into LDS.  The loads of chunk k+1
+//     (and its per-step scalars) are issued before chunk k is computed and land
+//     in registers, so their latency hides behind the arithmetic.
+//  2. Each thread reads its own two rows from LDS: row maxima, exponent sums,
+//     the importance ratio (float64, see device_common.hpp), rho and c.
 //  3. The recursion v_t - V(x_t) = delta_t + gamma_t c_t (v_{t+1} - V(x_{t+1}))
-//     (Remark 1) is an affine map per step.  A suffix scan across the 16
-//     threads of the lane's row composes the maps of the chunk; applying the
-//     result to the carry from the later chunk gives every v_t at once.
+//     (Remark 1) is an affine map per step.  A suffix scan across the row (DPP
+//     row shifts) composes the chunk's maps; applying them to the carry from
+//     the later chunk gives every v_t of the chunk at once.
 //  4. Advantages, d_values and the gradient row follow.  Gradient rows go
 //     through LDS so that the global stores are whole 16-byte vectors along the
 //     contiguous [t, b0:b0+LANES, :] runs.
+//
+// Workgroups whose lane tile is full and whose rows are 16-byte aligned take
+// the vector path above; a ragged last tile (or unaligned rows) copies element
+// by element without prefetching.
 #include <utility>
 
 #include "device_common.hpp"
@@ -31,8 +35,7 @@ namespace {
 
 constexpr int kL = 16;  // steps per chunk = threads per lane row
 
-// A native 16-byte vector: plain vector loads and stores, kept in registers
-// (HIP's v4u wrapper is copied through memory when carried across loops).
+// A native 16-byte vector: plain vector loads and stores, kept in registers.
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 // Calls f(std::integral_constant<int, i>) for i = 0..N-1, unrolled at compile
@@ -46,218 +49,233 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+// DPP row moves on a double (two 32-bit halves).  Lanes whose source falls
+// outside their row of 16 keep their own value.
+//   0x100 + k (row_shl:k): lane i of a row reads lane i+k;
+//   kRowShr15 (row_shr:15): lane 15 of a row reads lane 0.
+template <int kCtrl>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const unsigned long long u = __double_as_longlong(x);
+  int lo = static_cast<int>(u & 0xffffffffu);
+  int hi = static_cast<int>(u >> 32);
+  lo = __builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
+  hi = __builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
+  return __longlong_as_double(static_cast<long long>(
+      (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+constexpr int kRowShl1 = 0x101;
+constexpr int kRowShr15 = 0x11F;
+
+// exp(x) for x <= 0 from the hardware base-2 exponential.  The rounding error of
+// x*log2(e) is recovered with an FMA and applied as a first-order correction,
+// so the result keeps about the accuracy of the exp2 instruction itself
+// instead of losing |x| * 2^-24 relative.  Results below the normal range flush
+// to zero, which is harmless here: every term is added to a sum that is >= 1.
+__device__ __forceinline__ float exp_nonpos(float x) {
+  constexpr float kLog2e = 1.44269502162933349609375f;  // float(log2(e))
+  constexpr float kLog2eLo = 1.925963033500011079e-8f;  // log2(e) - kLog2e
+  constexpr float kLn2 = 0.693147180559945309f;
+  const float u = x * kLog2e;
+  const float du = fmaf(x, kLog2e, -u) + x * kLog2eLo;
+  const float p = __builtin_amdgcn_exp2f(u);
+  return fmaf(p, du * kLn2, p);
+}
+
 template <int A_, int LANES, typename In>
 struct Tile {
   static constexpr int A = A_;
-  static constexpr int NT = LANES * kL;                          // threads per workgroup
-  static constexpr int SEG = LANES * A_;                         // elements per time row
-  static constexpr int IN_ROW16 = SEG * int(sizeof(In)) / 16;    // 16-byte vectors per row, logits
-  static constexpr int OUT_ROW16 = SEG * 4 / 16;                 // 16-byte vectors per row, d_logits
+  static constexpr int NT = LANES * kL;                        // threads per workgroup
+  static constexpr int SEG = LANES * A_;                       // elements per time row
+  static constexpr int IN_ROW16 = SEG * int(sizeof(In)) / 16;  // 16-byte vectors per row, logits
+  static constexpr int OUT_ROW16 = SEG * 4 / 16;               // 16-byte vectors per row, d_logits
   static constexpr int IN_TILE16 = kL * IN_ROW16;
   static constexpr int OUT_TILE16 = kL * OUT_ROW16;
-  static constexpr int NV = (IN_TILE16 + NT - 1) / NT;  // prefetch vectors per thread per tensor
+  static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;     // vectors per thread, both tensors
+  static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;        // gradient vectors per thread
   static constexpr int LDS16 = (2 * IN_TILE16 > OUT_TILE16) ? 2 * IN_TILE16 : OUT_TILE16;
   static_assert((SEG * int(sizeof(In))) % 16 == 0, "logit rows must be whole 16-byte vectors");
   static_assert((SEG * 4) % 16 == 0, "gradient rows must be whole 16-byte vectors");
   static_assert(NT % kWave == 0 && NT <= 1024, "bad workgroup size");
 };
 
-template <int A_, int LANES, typename In, bool kGrad>
-__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a) {
+// Per-thread state carried along the chunk walk.
+struct Carry {
+  double V, v, A;  // V(x_{t+1}), v_{t+1}, v_{t+1} - V(x_{t+1}) at the later chunk's first step
+  double pg, base, ent;
+};
+
+template <int A_, int LANES, typename In, bool kGrad, bool kVec>
+__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& cy) {
   using S = Tile<A_, LANES, In>;
   constexpr int NT = S::NT;
-  __shared__ v4u lds[S::LDS16];
-  __shared__ double red_scratch[3 * (NT / kWave)];
   v4u* const lds_z = lds;
   v4u* const lds_y = lds + S::IN_TILE16;
 
   const int tid = threadIdx.x;
   const int lane_local = tid / kL;
-  const int s = tid % kL;  // step within the chunk
-  const int row_base = (tid % kWave) & ~(kL - 1);
+  const int s = tid % kL;
   const int64_t T = a.T, B = a.B;
   const int64_t b0 = static_cast<int64_t>(blockIdx.x) * LANES;
   const int64_t b = b0 + lane_local;
   const bool lane_ok = b < B;
-  const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);  // lanes present in this tile
-  // 16-byte copies need every [t, b0, :] run to start on a 16-byte boundary.
-  const bool vec = (nb == LANES) && ((B * A_ * int64_t(sizeof(In))) % 16 == 0) &&
-                   ((B * A_ * 4) % 16 == 0);
+  const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
   const int nchunks = static_cast<int>((T + kL - 1) / kL);
 
-  const char* zg = static_cast<const char*>(a.target_logits);
-  const char* yg = static_cast<const char*>(a.behaviour_logits);
-  const In* zg_e = static_cast<const In*>(a.target_logits);
-  const In* yg_e = static_cast<const In*>(a.behaviour_logits);
+  // Byte strides of one time row.
+  const int64_t in_row = B * A_ * int64_t(sizeof(In));
+  const int64_t out_row = B * A_ * 4;
+  const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
+  const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
+  char* const dg = reinterpret_cast<char*>(a.d_logits) + b0 * A_ * 4;
 
-  v4u pz[S::NV], py[S::NV];  // prefetched logits of the next chunk (vector path)
+  // Register prefetch (vector path): NV 16-byte vectors covering both tensors,
+  // plus this thread's action, reward, discount and value.
+  v4u pre[S::NV];
+  int32_t p_act = 0;
+  float p_r = 0.f, p_g = 0.f, p_V = 0.f;
 
-  auto chunk_t0 = [&](int k) -> int64_t { return T - static_cast<int64_t>(k + 1) * kL; };
-
-  // Issues the 16-byte loads of chunk k's logits into pz/py.
-#define VTRACE_PREFETCH(k_)                                                                 \
-  do {                                                                                      \
-    const int64_t pf_t0 = chunk_t0(k_);                                                     \
-    static_for<S::NV>([&](auto I) {                                                         \
-      constexpr int i = decltype(I)::value;                                                 \
-      const int idx = tid + i * NT;                                                         \
-      if (idx < S::IN_TILE16) {                                                             \
-        const int r = idx / S::IN_ROW16, c = idx % S::IN_ROW16;                             \
-        const int64_t t = pf_t0 + r;                                                        \
-        if (t >= 0) {                                                                       \
-          const int64_t off = (t * B + b0) * A_ * int64_t(sizeof(In)) + int64_t(c) * 16;    \
-          pz[i] = *reinterpret_cast<const v4u*>(zg + off);                                \
-          py[i] = *reinterpret_cast<const v4u*>(yg + off);                                \
-        }                                                                                   \
-      }                                                                                     \
-    });                                                                                     \
-  } while (0)
-
-  // Puts chunk k's logits into LDS, laid out [s][lane][j] like global memory.
-  auto commit_scalar = [&](int k) {
-    // Ragged lane tile or unaligned rows: element copies of what exists.
-    const int64_t t0 = chunk_t0(k);
-    In* lz = reinterpret_cast<In*>(lds_z);
-    In* ly = reinterpret_cast<In*>(lds_y);
-    for (int e = tid; e < kL * S::SEG; e += NT) {
-      const int r = e / S::SEG, c = e % S::SEG;
-      const int64_t t = t0 + r;
-      if (t >= 0 && c < nb * A_) {
-        const int64_t off = (t * B + b0) * A_ + c;
-        lz[e] = zg_e[off];
-        ly[e] = yg_e[off];
+  auto prefetch = [&](int k) {
+    const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+    const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row 0
+    static_for<S::NV>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      const int f = tid + i * NT;
+      if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) {
+        const bool is_y = f >= S::IN_TILE16;
+        const int g = is_y ? f - S::IN_TILE16 : f;
+        int r = g / S::IN_ROW16;
+        const int c = g % S::IN_ROW16;
+        r = r < neg ? neg : r;
+        const char* base = is_y ? yg : zg;
+        pre[i] = *reinterpret_cast<const v4u*>(base + (t0 + r) * in_row + c * 16);
       }
-    }
-  };
-
-  // Writes the chunk's gradient rows from LDS to global memory.
-  auto store_grads = [&](int k) {
-    const int64_t t0 = chunk_t0(k);
-    if (vec) {
-      char* dg = reinterpret_cast<char*>(a.d_logits);
-      for (int idx = tid; idx < S::OUT_TILE16; idx += NT) {
-        const int r = idx / S::OUT_ROW16, c = idx % S::OUT_ROW16;
-        const int64_t t = t0 + r;
-        if (t >= 0) {
-          const int64_t off = (t * B + b0) * A_ * 4 + int64_t(c) * 16;
-          *reinterpret_cast<v4u*>(dg + off) = lds[idx];
-        }
-      }
-    } else {
-      const float* lo = reinterpret_cast<const float*>(lds);
-      for (int e = tid; e < kL * S::SEG; e += NT) {
-        const int r = e / S::SEG, c = e % S::SEG;
-        const int64_t t = t0 + r;
-        if (t >= 0 && c < nb * A_) a.d_logits[(t * B + b0) * A_ + c] = lo[e];
-      }
+    });
+    int64_t t = t0 + s;
+    t = t < 0 ? 0 : t;
+    if (lane_ok) {
+      const int64_t idx = t * B + b;
+      p_act = a.actions[idx];
+      p_r = a.rewards[idx];
+      p_g = a.discounts[idx];
+      p_V = a.values[idx];
     }
   };
 
   const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
   const float ce = a.entropy_cost;
-  const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
-  // Carries from the first step of the later chunk: V(x_{t+1}), v_{t+1}, v_{t+1} - V(x_{t+1}).
-  double carry_V = boot, carry_v = boot, carry_A = 0.0;
-  double acc_pg = 0.0, acc_base = 0.0, acc_ent = 0.0;
 
-  if (vec) VTRACE_PREFETCH(0);
+  if constexpr (kVec) prefetch(0);
   for (int k = 0; k < nchunks; ++k) {
-    const int64_t t = chunk_t0(k) + s;
+    const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+    const int64_t t = t0 + s;
     const bool step_ok = lane_ok && t >= 0;
     const int64_t idx = t * B + b;
 
-    __syncthreads();  // previous chunk is done with LDS
-    if (vec) {
+    __syncthreads();  // the previous chunk is done with LDS
+    int32_t act;
+    float r32, g32, V32;
+    if constexpr (kVec) {
       static_for<S::NV>([&](auto I) {
         constexpr int i = decltype(I)::value;
-        const int li = tid + i * NT;
-        if (li < S::IN_TILE16) {
-          lds_z[li] = pz[i];
-          lds_y[li] = py[i];
-        }
+        const int f = tid + i * NT;
+        if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) lds[f] = pre[i];
       });
+      act = p_act;
+      r32 = p_r;
+      g32 = p_g;
+      V32 = p_V;
+      __syncthreads();
+      if (k + 1 < nchunks) prefetch(k + 1);
     } else {
-      commit_scalar(k);
+      In* lz = reinterpret_cast<In*>(lds_z);
+      In* ly = reinterpret_cast<In*>(lds_y);
+      for (int e = tid; e < kL * S::SEG; e += NT) {
+        const int rr = e / S::SEG, c = e % S::SEG;
+        const int64_t te = t0 + rr;
+        if (te >= 0 && c < nb * A_) {
+          const int64_t off = (te * B + b0) * A_ + c;
+          lz[e] = static_cast<const In*>(a.target_logits)[off];
+          ly[e] = static_cast<const In*>(a.behaviour_logits)[off];
+        }
+      }
+      act = 0;
+      r32 = g32 = V32 = 0.f;
+      if (step_ok) {
+        act = a.actions[idx];
+        r32 = a.rewards[idx];
+        g32 = a.discounts[idx];
+        V32 = a.values[idx];
+      }
+      __syncthreads();
     }
-    // Per-step scalars of this thread.
-    int32_t act = 0;
-    double r = 0.0, g = 0.0, V = 0.0;
-    if (step_ok) {
-      act = a.actions[idx];
-      r = a.rewards[idx];
-      g = a.discounts[idx];
-      V = a.values[idx];
-    }
-    __syncthreads();
-    if (vec && k + 1 < nchunks) VTRACE_PREFETCH(k + 1);
+    if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
 
-    // Own rows from LDS.
+    // This thread's rows.
     const In* zr = reinterpret_cast<const In*>(lds_z) + (s * LANES + lane_local) * A_;
     const In* yr = reinterpret_cast<const In*>(lds_y) + (s * LANES + lane_local) * A_;
-    float dz[A_], e[A_];
-    float mz = -INFINITY, my = -INFINITY, za = 0.f, ya = 0.f;
-#pragma unroll
-    for (int j = 0; j < A_; ++j) {
-      dz[j] = logit_to_float(zr[j]);
-      mz = fmaxf(mz, dz[j]);
-      if (j == act) za = dz[j];
-    }
-    double sy = 0.0;
-    {
-      float yv[A_];
-#pragma unroll
-      for (int j = 0; j < A_; ++j) {
-        yv[j] = logit_to_float(yr[j]);
-        my = fmaxf(my, yv[j]);
-        if (j == act) ya = yv[j];
-      }
-#pragma unroll
-      for (int j = 0; j < A_; ++j) sy += static_cast<double>(expf(yv[j] - my));
-    }
-    double sz = 0.0;
-    float ed = 0.f, ea = 0.f;
-#pragma unroll
-    for (int j = 0; j < A_; ++j) {
-      dz[j] -= mz;
-      e[j] = expf(dz[j]);
-      sz += static_cast<double>(e[j]);
-      ed += e[j] * dz[j];
-      if (j == act) ea = e[j];
-    }
-
     const bool act_ok = act >= 0 && act < A_;
+    const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
-    const double ratio = act_ok ? importance_ratio(za, mz, ya, my, sz, sy) : NAN;
+    const float za = logit_to_float(zr[act_c]);
+    const float ya = logit_to_float(yr[act_c]);
+
+    float e[A_];
+    float mz = logit_to_float(zr[0]);
+#pragma unroll
+    for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
+    double sz = 0.0;
+    float ed = 0.f;
+#pragma unroll
+    for (int j = 0; j < A_; ++j) {
+      const float d = logit_to_float(zr[j]) - mz;
+      e[j] = exp_nonpos(d);
+      sz += static_cast<double>(e[j]);
+      ed = fmaf(e[j], d, ed);
+    }
+    float my = logit_to_float(yr[0]);
+#pragma unroll
+    for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
+    double sy = 0.0;
+#pragma unroll
+    for (int j = 0; j < A_; ++j) sy += static_cast<double>(exp_nonpos(logit_to_float(yr[j]) - my));
+
+    const double inv_sz = 1.0 / sz;
+    const double dza = static_cast<double>(za) - static_cast<double>(mz);
+    const double dya = static_cast<double>(ya) - static_cast<double>(my);
+    const double ratio = act_ok ? exp(dza - dya) * (sy * inv_sz) : NAN;
     const double rho = clip_above(ratio, rho_bar);
     const double c = lam * clip_above(ratio, c_bar);
 
-    // V(x_{t+1}) from the next thread of the row, or the later chunk's carry.
-    double V_next = __shfl_down(V, 1, kL);
-    if (s == kL - 1) V_next = carry_V;
+    const double r = r32, g = g32, V = V32;
+    double V_next = dpp_f64<kRowShl1>(V);
+    if (s == kL - 1) V_next = cy.V;
     const double delta = rho * (r + g * V_next - V);
 
-    // Suffix scan of the affine maps x -> delta_t + (gamma_t c_t) x over the row:
-    // (G, D) composes steps t..15 of the chunk.
+    // Suffix scan over the row.  Step 15 first absorbs the carry from the later
+    // chunk, so that after the scan D holds v_t - V(x_t) on every thread:
+    // (G, D) composes the maps of steps s..15 applied to that carry.
     double G = g * c, D = delta;
-#pragma unroll
-    for (int off = 1; off < kL; off <<= 1) {
-      const double Gn = __shfl_down(G, off, kL);
-      const double Dn = __shfl_down(D, off, kL);
+    if (s == kL - 1) D = fma(G, cy.A, D);
+    static_for<4>([&](auto I) {
+      constexpr int off = 1 << decltype(I)::value;
+      const double Gn = dpp_f64<0x100 + off>(G);
+      const double Dn = dpp_f64<0x100 + off>(D);
       if (s + off < kL) {
-        D = D + G * Dn;
+        D = fma(G, Dn, D);
         G = G * Gn;
       }
-    }
-    const double A_t = D + G * carry_A;  // v_t - V(x_t)
+    });
+    const double A_t = D;  // v_t - V(x_t)
     const double v_t = V + A_t;
-    double v_next = __shfl_down(v_t, 1, kL);
-    if (s == kL - 1) v_next = carry_v;
+    double v_next = dpp_f64<kRowShl1>(v_t);
+    if (s == kL - 1) v_next = cy.v;
     const double adv = rho * (r + g * v_next - V);
 
-    // Carries for the earlier chunk come from the row's first thread.
-    carry_A = __shfl(A_t, row_base, kWave);
-    carry_v = __shfl(v_t, row_base, kWave);
-    carry_V = __shfl(V, row_base, kWave);
+    // The row's first step becomes the carry of the earlier chunk, held by the
+    // row's last thread, the only one that reads it.
+    cy.A = dpp_f64<kRowShr15>(A_t);
+    cy.v = dpp_f64<kRowShr15>(v_t);
+    cy.V = dpp_f64<kRowShr15>(V);
 
     if (step_ok) {
       if (a.vs) a.vs[idx] = static_cast<float>(v_t);
@@ -265,53 +283,96 @@ __global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a) {
     }
 
     if constexpr (kGrad) {
-      const float szf = static_cast<float>(sz);
-      const float inv = 1.0f / szf;
-      const float log_s = logf(szf);
+      const float inv = static_cast<float>(inv_sz);
+      const float log_s = logf(static_cast<float>(sz));
       const float H = log_s - ed * inv;
-      const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) / sz);
+      // log pi_j + H = (z_j - mz) - log_s + H = z_j - K
+      const float K = mz + log_s - H;
       const float adv32 = static_cast<float>(adv);
+      const float ea = exp_nonpos(za - mz);  // the same value as e[act]
+      const float pa = ea * inv;
+      // Taken action: adv*(pi_a - 1), with 1 - pi_a = (s - e_a)/s free of cancellation.
+      const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) * inv_sz);
+      const float out_a = -adv32 * one_minus_pa + ce * pa * (za - K);
+      if (step_ok) {
+        a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+        const double log_pa = act_ok ? dza - static_cast<double>(log_s) : NAN;
+        cy.pg += -adv * log_pa;
+        cy.base += 0.5 * A_t * A_t;
+        cy.ent += -static_cast<double>(H);
+      }
       float out[A_];
 #pragma unroll
       for (int j = 0; j < A_; ++j) {
         const float p = e[j] * inv;
-        const float pg_term = (j == act) ? -one_minus_pa : p;
-        out[j] = adv32 * pg_term + ce * p * ((dz[j] - log_s) + H);
+        out[j] = fmaf(adv32, p, ce * p * (logit_to_float(zr[j]) - K));
       }
-      if (step_ok) {
-        a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
-        const double log_pa = act_ok ? static_cast<double>(za - mz) - static_cast<double>(log_s) : NAN;
-        acc_pg += -adv * log_pa;
-        acc_base += 0.5 * A_t * A_t;
-        acc_ent += -static_cast<double>(H);
-      }
-      __syncthreads();  // all rows read: LDS now holds the gradient tile
+      __syncthreads();  // every row has been read: LDS now takes the gradient tile
       float* lo = reinterpret_cast<float*>(lds) + (s * LANES + lane_local) * A_;
 #pragma unroll
       for (int j = 0; j < A_; ++j) lo[j] = out[j];
+      lo[act_c] = act_ok ? out_a : NAN;
       __syncthreads();
-      store_grads(k);
+      if constexpr (kVec) {
+        const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
+        static_for<S::NO>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          const int f = tid + i * NT;
+          if (i * NT + NT <= S::OUT_TILE16 || f < S::OUT_TILE16) {
+            const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
+            if (rr >= neg)
+              *reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16) = lds[f];
+          }
+        });
+      } else {
+        const float* lf = reinterpret_cast<const float*>(lds);
+        for (int e2 = tid; e2 < kL * S::SEG; e2 += NT) {
+          const int rr = e2 / S::SEG, cc = e2 % S::SEG;
+          const int64_t te = t0 + rr;
+          if (te >= 0 && cc < nb * A_) a.d_logits[(te * B + b0) * A_ + cc] = lf[e2];
+        }
+      }
     }
   }
+}
 
-#undef VTRACE_PREFETCH
+template <int A_, int LANES, typename In, bool kGrad>
+__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t num_vec_blocks) {
+  using S = Tile<A_, LANES, In>;
+  constexpr int NT = S::NT;
+  __shared__ v4u lds[S::LDS16];
+  __shared__ double red_scratch[3 * (NT / kWave)];
+
+  const int lane_local = threadIdx.x / kL;
+  const int s = threadIdx.x % kL;
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * LANES + lane_local;
+  const bool lane_ok = b < a.B;
+  const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
+  Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
+
+  if (static_cast<int64_t>(blockIdx.x) < num_vec_blocks)
+    chunk_walk<A_, LANES, In, kGrad, true>(a, lds, cy);
+  else
+    chunk_walk<A_, LANES, In, kGrad, false>(a, lds, cy);
+
   if constexpr (kGrad) {
     // Per-lane totals over the row (fixed butterfly order), then the workgroup.
+    double pg = cy.pg, base = cy.base, ent = cy.ent;
 #pragma unroll
     for (int off = kL / 2; off > 0; off >>= 1) {
-      acc_pg += __shfl_xor(acc_pg, off, kL);
-      acc_base += __shfl_xor(acc_base, off, kL);
-      acc_ent += __shfl_xor(acc_ent, off, kL);
+      pg += __shfl_xor(pg, off, kL);
+      base += __shfl_xor(base, off, kL);
+      ent += __shfl_xor(ent, off, kL);
     }
-    acc_base *= a.baseline_cost;
-    acc_ent *= a.entropy_cost;
+    base *= a.baseline_cost;
+    ent *= a.entropy_cost;
     if (s == 0 && lane_ok && a.lane_losses) {
-      a.lane_losses[3 * b + 0] = static_cast<float>(acc_pg);
-      a.lane_losses[3 * b + 1] = static_cast<float>(acc_base);
-      a.lane_losses[3 * b + 2] = static_cast<float>(acc_ent);
+      a.lane_losses[3 * b + 0] = static_cast<float>(pg);
+      a.lane_losses[3 * b + 1] = static_cast<float>(base);
+      a.lane_losses[3 * b + 2] = static_cast<float>(ent);
     }
-    if (s != 0 || !lane_ok) acc_pg = acc_base = acc_ent = 0.0;
-    finish_losses<NT>(a, acc_pg, acc_base, acc_ent, red_scratch);
+    if (s != 0 || !lane_ok) pg = base = ent = 0.0;
+    finish_losses<NT>(a, pg, base, ent, red_scratch);
   }
 }
 
@@ -319,12 +380,17 @@ template <int A_, int LANES, typename In>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg) {
   const int64_t blocks = (a.B + LANES - 1) / LANES;
   *nwg = blocks;
+  // Vector path: full lane tiles whose time rows start on 16-byte boundaries.
+  const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
+  const int64_t out_row = a.B * A_ * 4;
+  const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
+  const int64_t vec_blocks = aligned ? a.B / LANES : 0;
   if (mode == Mode::LossGrad)
     hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, true>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(LANES * kL), 0, st, a);
+                       dim3(LANES * kL), 0, st, a, vec_blocks);
   else
     hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, false>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(LANES * kL), 0, st, a);
+                       dim3(LANES * kL), 0, st, a, vec_blocks);
   return hipGetLastError();
 }
 
@@ -332,8 +398,8 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
 
 bool tiled_supported(const StepArgs& a, LogitsType) { return a.A == 9 || a.A == 18; }
 
-// Lanes per workgroup: the smallest count whose [t, b0:b0+LANES, :] run of
-// logits is 1152 bytes (nine 128-byte lines).
+// Lanes per workgroup: the count whose [t, b0:b0+LANES, :] run of logits is
+// 1152 bytes (nine 128-byte lines).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups) {
   if (lt == LogitsType::F32) {

@@ -263,6 +263,10 @@ def test_kernels_agree(monkeypatch):
         monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
         b = run_loss_grad(dev, p)
         monkeypatch.delenv("VTRACE_KERNEL")
-        for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses", "losses"):
+        for name in ("vs", "pg_advantages", "d_values", "d_logits"):
             assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
                          np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
+        # loss sums cancel (advantages of both signs): the oracle's tolerance
+        for name in ("lane_losses", "losses"):
+            assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
+                         np_out(getattr(b, name)))
