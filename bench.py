@@ -43,7 +43,40 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run plain device-to-device copies of MIB MiB (the reference "
+                         "kernel for scaling HBM byte counters), then exit")
     return ap.parse_args()
+
+
+def calibrate_copy(mib, reps):
+    """Plain copies of a known size: what a byte counter reads for them calibrates
+    the counter (bytes counted per byte moved)."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_ms = e0.elapsed_time(e1) / reps
+    # a pure read for comparison: a sum over the same buffer
+    src.sum()
+    e0.record()
+    for _ in range(reps):
+        src.sum()
+    e1.record()
+    torch.cuda.synchronize()
+    read_ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"calibrate_copy_bytes_read": n * 4, "calibrate_copy_bytes_written": n * 4,
+                      "copies": reps + 1, "copy_ms": copy_ms,
+                      "copy_GBps_read_plus_write": 2 * n * 4 / copy_ms / 1e6,
+                      "sum_read_GBps": n * 4 / read_ms / 1e6}), flush=True)
 
 
 def kernel_source_digest() -> str:
@@ -78,17 +111,20 @@ def to_device(tr, torch, np):
                 bootstrap_value=d(tr.bootstrap_value))
 
 
-def stored_traffic(per_launch_kernel_ms):
-    """HBM bytes per launch from committed rocprofv3 counter runs, or None when
-    they are missing or were taken on different kernel sources."""
+def stored_traffic(avg_kernel_ms):
+    """Counted HBM traffic of one launch, from committed rocprofv3 FETCH_SIZE and
+    WRITE_SIZE runs scaled by the same counters' readings for a plain copy of
+    known size, as (GB/s over this run's average launch time, bytes per launch).
+    None when the counters are missing or were taken on other kernel sources."""
     try:
         with open(COUNTERS_FILE) as fh:
             c = json.load(fh)
     except (OSError, ValueError):
-        return None
+        return None, None
     if c.get("kernel_source_digest") != kernel_source_digest():
-        return None
-    return c.get("hbm_bytes_per_launch")
+        return None, None
+    nbytes = c["hbm_bytes_per_launch"]
+    return nbytes / (avg_kernel_ms * 1e-3) / 1e9, nbytes
 
 
 def cpu_baseline(tr, p, target_s):
@@ -137,6 +173,9 @@ def main():
               "independent, so the batch axis would shard across GPUs with no communication "
               "except a 4-float loss all-reduce.", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy, max(1, args.steps))
+        return
     if args.kernel == "lane_serial":
         os.environ["VTRACE_KERNEL"] = "lane_serial"
 
@@ -198,7 +237,9 @@ def main():
           f"{np.median(kernel_ms):.4f}); wall {ms_per_step:.4f} ms/step; {achieved:.1f} GB/s "
           f"algorithmic; losses {losses}", file=sys.stderr, flush=True)
 
-    traffic = stored_traffic(avg_kernel_ms)
+    is_counted_workload = (args.config == 4 and args.params == 0 and not args.bf16
+                           and args.kernel == "auto")
+    traffic, traffic_bytes = stored_traffic(avg_kernel_ms) if is_counted_workload else (None, None)
     result = {
         "metric": METRIC,
         "value": steps_per_s,
@@ -222,6 +263,8 @@ def main():
             "seed": tr.seed,
         },
         "kernel_ms_avg": avg_kernel_ms,
+        "alg_bytes_per_launch": alg_bytes,
+        "traffic_bytes_per_launch": traffic_bytes,
         "kernel_ms_min": float(kernel_ms.min()),
         "alg_bytes_per_step": per_step,
         "roofline": {

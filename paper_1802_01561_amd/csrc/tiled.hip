@@ -9,8 +9,11 @@
 //
 // Data path per chunk.
 //  1. For each t the chunk's logits are one contiguous run of LANES*A elements
-//     (1152 bytes for every supported shape: nine 128-byte lines).  Threads copy
-//     both tensors' runs with 16-byte loads into LDS.  The loads of chunk k+1
+//     (1152 bytes for fp32 logits: nine 128-byte lines).  Threads copy both
+//     tensors' runs with 16-byte loads into LDS.  These whole-line logit loads
+//     and the gradient stores are used once, so they carry the non-temporal
+//     hint; the [T,B] scalars, whose 64-byte halves neighbouring workgroups
+//     share in L2, do not.  The loads of chunk k+1
 //     (and its per-step scalars) are issued before chunk k is computed and land
 //     in registers, so their latency hides behind the arithmetic.
 //  2. Each thread reads its own two rows from LDS: row maxima, exponent sums,
@@ -66,19 +69,11 @@ __device__ __forceinline__ double dpp_f64(double x) {
 constexpr int kRowShl1 = 0x101;
 constexpr int kRowShr15 = 0x11F;
 
-// exp(x) for x <= 0 from the hardware base-2 exponential.  The rounding error of
-// x*log2(e) is recovered with an FMA and applied as a first-order correction,
-// so the result keeps about the accuracy of the exp2 instruction itself
-// instead of losing |x| * 2^-24 relative.  Results below the normal range flush
-// to zero, which is harmless here: every term is added to a sum that is >= 1.
-__device__ __forceinline__ float exp_nonpos(float x) {
-  constexpr float kLog2e = 1.44269502162933349609375f;  // float(log2(e))
-  constexpr float kLog2eLo = 1.925963033500011079e-8f;  // log2(e) - kLog2e
-  constexpr float kLn2 = 0.693147180559945309f;
-  const float u = x * kLog2e;
-  const float du = fmaf(x, kLog2e, -u) + x * kLog2eLo;
-  const float p = __builtin_amdgcn_exp2f(u);
-  return fmaf(p, du * kLn2, p);
+// e^x from the hardware base-2 exponential (about one ulp; results below the
+// normal range flush to zero, harmless where every term joins a sum >= 1).
+__device__ __forceinline__ float exp_fast(float x) {
+  constexpr float kLog2e = 1.44269504088896340736f;
+  return __builtin_amdgcn_exp2f(x * kLog2e);
 }
 
 template <int A_, int LANES, typename In>
@@ -88,11 +83,19 @@ struct Tile {
   static constexpr int SEG = LANES * A_;                       // elements per time row
   static constexpr int IN_ROW16 = SEG * int(sizeof(In)) / 16;  // 16-byte vectors per row, logits
   static constexpr int OUT_ROW16 = SEG * 4 / 16;               // 16-byte vectors per row, d_logits
-  static constexpr int IN_TILE16 = kL * IN_ROW16;
+  // LDS rows are padded by one 16-byte vector: without it every step of a lane
+  // would read the same banks (a row is a multiple of 128 bytes).
+  static constexpr int IN_PITCH16 = IN_ROW16 + 1;
+  static constexpr int OUT_PITCH16 = OUT_ROW16 + 1;
+  static constexpr int IN_TILE16 = kL * IN_ROW16;    // vectors per tensor and chunk
   static constexpr int OUT_TILE16 = kL * OUT_ROW16;
-  static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;     // vectors per thread, both tensors
-  static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;        // gradient vectors per thread
-  static constexpr int LDS16 = (2 * IN_TILE16 > OUT_TILE16) ? 2 * IN_TILE16 : OUT_TILE16;
+  static constexpr int IN_LDS16 = kL * IN_PITCH16;   // LDS footprint per tensor
+  static constexpr int OUT_LDS16 = kL * OUT_PITCH16;
+  static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;  // vectors per thread, both tensors
+  static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;     // gradient vectors per thread
+  static constexpr int LDS16 = (2 * IN_LDS16 > OUT_LDS16) ? 2 * IN_LDS16 : OUT_LDS16;
+  static constexpr int IN_PITCH = IN_PITCH16 * 16 / int(sizeof(In));  // elements per LDS row
+  static constexpr int OUT_PITCH = OUT_PITCH16 * 4;                    // floats per LDS row
   static_assert((SEG * int(sizeof(In))) % 16 == 0, "logit rows must be whole 16-byte vectors");
   static_assert((SEG * 4) % 16 == 0, "gradient rows must be whole 16-byte vectors");
   static_assert(NT % kWave == 0 && NT <= 1024, "bad workgroup size");
@@ -104,18 +107,93 @@ struct Carry {
   double pg, base, ent;
 };
 
-template <int A_, int LANES, typename In, bool kGrad, bool kVec>
-__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& cy) {
+// Row statistics of one step: what the rest of the step needs from the logits.
+struct RowStats {
+  double ratio;       // pi(a|x) / mu(a|x)
+  float inv_s;        // 1 / sum_j exp(z_j - m_z)
+  float log_s;        // log of that sum
+  float H;            // entropy of pi
+  float one_minus_pa; // 1 - pi(a|x), formed without cancellation
+  float e_a;          // exp(z_a - m_z)
+  float mz;
+};
+
+// kPrecise: the importance ratio feeds products of c over many steps (lambda *
+// c_bar > 1) or is left unclipped above 1 (rho_bar > 1), so errors in it are
+// amplified; the exponent sums are then formed from float64 exponentials of
+// exact float64 differences.  Otherwise every weight is at most 1, nothing is
+// amplified, and float32 exponentials are accurate enough.
+template <int A_, bool kPrecise, typename In>
+__device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
+                                              float (&e)[A_]) {
+  RowStats st;
+  const float za = logit_to_float(zr[act_c]);
+  const float ya = logit_to_float(yr[act_c]);
+  float mz = logit_to_float(zr[0]);
+#pragma unroll
+  for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
+  float my = logit_to_float(yr[0]);
+#pragma unroll
+  for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
+  st.mz = mz;
+  float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
+  if constexpr (kPrecise) {
+    double sz = 0.0, sy = 0.0;
+#pragma unroll
+    for (int j = 0; j < A_; ++j) {
+      const double d = static_cast<double>(logit_to_float(zr[j])) - static_cast<double>(mz);
+      const double x = exp(d);
+      sz += x;
+      e[j] = static_cast<float>(x);
+      ed = fmaf(e[j], static_cast<float>(d), ed);
+    }
+#pragma unroll
+    for (int j = 0; j < A_; ++j)
+      sy += exp(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
+    const double inv = 1.0 / sz;
+    const double dza = static_cast<double>(za) - static_cast<double>(mz);
+    const double dya = static_cast<double>(ya) - static_cast<double>(my);
+    const double ea = exp(dza);
+    st.ratio = act_ok ? exp(dza - dya) * (sy * inv) : NAN;
+    st.inv_s = static_cast<float>(inv);
+    st.log_s = static_cast<float>(log(sz));
+    st.one_minus_pa = static_cast<float>((sz - ea) * inv);
+    st.e_a = static_cast<float>(ea);
+  } else {
+    float sz = 0.f, sy = 0.f;
+#pragma unroll
+    for (int j = 0; j < A_; ++j) {
+      const float d = logit_to_float(zr[j]) - mz;
+      e[j] = exp_fast(d);
+      sz += e[j];
+      ed = fmaf(e[j], d, ed);
+    }
+#pragma unroll
+    for (int j = 0; j < A_; ++j) sy += exp_fast(logit_to_float(yr[j]) - my);
+    const float inv = __builtin_amdgcn_rcpf(sz);
+    const float ea = exp_fast(za - mz);
+    st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
+    st.inv_s = inv;
+    st.log_s = __logf(sz);
+    st.one_minus_pa = (sz - ea) * inv;
+    st.e_a = ea;
+  }
+  st.H = st.log_s - ed * st.inv_s;
+  return st;
+}
+
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kVec>
+__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t tile, Carry& cy) {
   using S = Tile<A_, LANES, In>;
   constexpr int NT = S::NT;
   v4u* const lds_z = lds;
-  v4u* const lds_y = lds + S::IN_TILE16;
+  v4u* const lds_y = lds + S::IN_LDS16;
 
   const int tid = threadIdx.x;
   const int lane_local = tid / kL;
   const int s = tid % kL;
   const int64_t T = a.T, B = a.B;
-  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * LANES;
+  const int64_t b0 = tile * LANES;
   const int64_t b = b0 + lane_local;
   const bool lane_ok = b < B;
   const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
@@ -147,7 +225,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
         const int c = g % S::IN_ROW16;
         r = r < neg ? neg : r;
         const char* base = is_y ? yg : zg;
-        pre[i] = *reinterpret_cast<const v4u*>(base + (t0 + r) * in_row + c * 16);
+        pre[i] = __builtin_nontemporal_load(
+            reinterpret_cast<const v4u*>(base + (t0 + r) * in_row + c * 16));
       }
     });
     int64_t t = t0 + s;
@@ -178,7 +257,12 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
       static_for<S::NV>([&](auto I) {
         constexpr int i = decltype(I)::value;
         const int f = tid + i * NT;
-        if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) lds[f] = pre[i];
+        if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) {
+          const bool is_y = f >= S::IN_TILE16;
+          const int g = is_y ? f - S::IN_TILE16 : f;
+          const int r = g / S::IN_ROW16, c = g % S::IN_ROW16;
+          lds[(is_y ? S::IN_LDS16 : 0) + r * S::IN_PITCH16 + c] = pre[i];
+        }
       });
       act = p_act;
       r32 = p_r;
@@ -194,8 +278,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
         const int64_t te = t0 + rr;
         if (te >= 0 && c < nb * A_) {
           const int64_t off = (te * B + b0) * A_ + c;
-          lz[e] = static_cast<const In*>(a.target_logits)[off];
-          ly[e] = static_cast<const In*>(a.behaviour_logits)[off];
+          lz[rr * S::IN_PITCH + c] = static_cast<const In*>(a.target_logits)[off];
+          ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
         }
       }
       act = 0;
@@ -211,40 +295,15 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
     if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
 
     // This thread's rows.
-    const In* zr = reinterpret_cast<const In*>(lds_z) + (s * LANES + lane_local) * A_;
-    const In* yr = reinterpret_cast<const In*>(lds_y) + (s * LANES + lane_local) * A_;
+    const In* zr = reinterpret_cast<const In*>(lds_z) + s * S::IN_PITCH + lane_local * A_;
+    const In* yr = reinterpret_cast<const In*>(lds_y) + s * S::IN_PITCH + lane_local * A_;
     const bool act_ok = act >= 0 && act < A_;
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
-    const float za = logit_to_float(zr[act_c]);
-    const float ya = logit_to_float(yr[act_c]);
-
     float e[A_];
-    float mz = logit_to_float(zr[0]);
-#pragma unroll
-    for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
-    double sz = 0.0;
-    float ed = 0.f;
-#pragma unroll
-    for (int j = 0; j < A_; ++j) {
-      const float d = logit_to_float(zr[j]) - mz;
-      e[j] = exp_nonpos(d);
-      sz += static_cast<double>(e[j]);
-      ed = fmaf(e[j], d, ed);
-    }
-    float my = logit_to_float(yr[0]);
-#pragma unroll
-    for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
-    double sy = 0.0;
-#pragma unroll
-    for (int j = 0; j < A_; ++j) sy += static_cast<double>(exp_nonpos(logit_to_float(yr[j]) - my));
-
-    const double inv_sz = 1.0 / sz;
-    const double dza = static_cast<double>(za) - static_cast<double>(mz);
-    const double dya = static_cast<double>(ya) - static_cast<double>(my);
-    const double ratio = act_ok ? exp(dza - dya) * (sy * inv_sz) : NAN;
-    const double rho = clip_above(ratio, rho_bar);
-    const double c = lam * clip_above(ratio, c_bar);
+    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, e);
+    const double rho = clip_above(st.ratio, rho_bar);
+    const double c = lam * clip_above(st.ratio, c_bar);
 
     const double r = r32, g = g32, V = V32;
     double V_next = dpp_f64<kRowShl1>(V);
@@ -283,32 +342,28 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
     }
 
     if constexpr (kGrad) {
-      const float inv = static_cast<float>(inv_sz);
-      const float log_s = logf(static_cast<float>(sz));
-      const float H = log_s - ed * inv;
-      // log pi_j + H = (z_j - mz) - log_s + H = z_j - K
-      const float K = mz + log_s - H;
+      // d_logits_j = adv (pi_j - 1[j=a]) + ce pi_j (log pi_j + H), where
+      // log pi_j + H = z_j - K.  For j != a this is e_j (alpha + beta z_j).
+      const float K = st.mz + st.log_s - st.H;
       const float adv32 = static_cast<float>(adv);
-      const float ea = exp_nonpos(za - mz);  // the same value as e[act]
-      const float pa = ea * inv;
-      // Taken action: adv*(pi_a - 1), with 1 - pi_a = (s - e_a)/s free of cancellation.
-      const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) * inv_sz);
-      const float out_a = -adv32 * one_minus_pa + ce * pa * (za - K);
+      const float beta = st.inv_s * ce;
+      const float alpha = st.inv_s * adv32 - beta * K;
+      const float za = logit_to_float(zr[act_c]);
+      const float out_a =
+          -adv32 * st.one_minus_pa + ce * (st.e_a * st.inv_s) * (za - K);
       if (step_ok) {
         a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
-        const double log_pa = act_ok ? dza - static_cast<double>(log_s) : NAN;
+        const double log_pa =
+            act_ok ? static_cast<double>(za - st.mz) - static_cast<double>(st.log_s) : NAN;
         cy.pg += -adv * log_pa;
         cy.base += 0.5 * A_t * A_t;
-        cy.ent += -static_cast<double>(H);
+        cy.ent += -static_cast<double>(st.H);
       }
       float out[A_];
 #pragma unroll
-      for (int j = 0; j < A_; ++j) {
-        const float p = e[j] * inv;
-        out[j] = fmaf(adv32, p, ce * p * (logit_to_float(zr[j]) - K));
-      }
+      for (int j = 0; j < A_; ++j) out[j] = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
       __syncthreads();  // every row has been read: LDS now takes the gradient tile
-      float* lo = reinterpret_cast<float*>(lds) + (s * LANES + lane_local) * A_;
+      float* lo = reinterpret_cast<float*>(lds) + s * S::OUT_PITCH + lane_local * A_;
 #pragma unroll
       for (int j = 0; j < A_; ++j) lo[j] = out[j];
       lo[act_c] = act_ok ? out_a : NAN;
@@ -321,7 +376,9 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
           if (i * NT + NT <= S::OUT_TILE16 || f < S::OUT_TILE16) {
             const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
             if (rr >= neg)
-              *reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16) = lds[f];
+              __builtin_nontemporal_store(
+                  lds[rr * S::OUT_PITCH16 + cc],
+                  reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
           }
         });
       } else {
@@ -329,31 +386,43 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, Carry& c
         for (int e2 = tid; e2 < kL * S::SEG; e2 += NT) {
           const int rr = e2 / S::SEG, cc = e2 % S::SEG;
           const int64_t te = t0 + rr;
-          if (te >= 0 && cc < nb * A_) a.d_logits[(te * B + b0) * A_ + cc] = lf[e2];
+          if (te >= 0 && cc < nb * A_)
+            a.d_logits[(te * B + b0) * A_ + cc] = lf[rr * S::OUT_PITCH + cc];
         }
       }
     }
   }
 }
 
-template <int A_, int LANES, typename In, bool kGrad>
-__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t num_vec_blocks) {
+// Workgroups are handed to the 8 XCDs round-robin; number the lane tiles so
+// that neighbouring tiles (which share 128-byte lines of the [T,B] arrays) run
+// on the same XCD and meet in its L2.
+__device__ __forceinline__ int64_t xcd_tile(int64_t block, int64_t nblocks) {
+  constexpr int64_t kXcd = 8;
+  const int64_t per = nblocks / kXcd;
+  if (block >= per * kXcd) return block;
+  return (block % kXcd) * per + block / kXcd;
+}
+
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise>
+__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t num_vec_tiles) {
   using S = Tile<A_, LANES, In>;
   constexpr int NT = S::NT;
   __shared__ v4u lds[S::LDS16];
   __shared__ double red_scratch[3 * (NT / kWave)];
 
+  const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const int lane_local = threadIdx.x / kL;
   const int s = threadIdx.x % kL;
-  const int64_t b = static_cast<int64_t>(blockIdx.x) * LANES + lane_local;
+  const int64_t b = tile * LANES + lane_local;
   const bool lane_ok = b < a.B;
   const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
   Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
 
-  if (static_cast<int64_t>(blockIdx.x) < num_vec_blocks)
-    chunk_walk<A_, LANES, In, kGrad, true>(a, lds, cy);
+  if (tile < num_vec_tiles)
+    chunk_walk<A_, LANES, In, kGrad, kPrecise, true>(a, lds, tile, cy);
   else
-    chunk_walk<A_, LANES, In, kGrad, false>(a, lds, cy);
+    chunk_walk<A_, LANES, In, kGrad, kPrecise, false>(a, lds, tile, cy);
 
   if constexpr (kGrad) {
     // Per-lane totals over the row (fixed butterfly order), then the workgroup.
@@ -376,6 +445,18 @@ __global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t nu
   }
 }
 
+template <int A_, int LANES, typename In, bool kGrad>
+void launch_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int64_t vec_tiles) {
+  // float32 ratios suffice when no weight can exceed 1.
+  const bool precise = !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+  if (precise)
+    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, true>), dim3(blocks), dim3(LANES * kL),
+                       0, st, a, vec_tiles);
+  else
+    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, false>), dim3(blocks), dim3(LANES * kL),
+                       0, st, a, vec_tiles);
+}
+
 template <int A_, int LANES, typename In>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg) {
   const int64_t blocks = (a.B + LANES - 1) / LANES;
@@ -384,13 +465,11 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
   const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
   const int64_t out_row = a.B * A_ * 4;
   const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
-  const int64_t vec_blocks = aligned ? a.B / LANES : 0;
+  const int64_t vec_tiles = aligned ? a.B / LANES : 0;
   if (mode == Mode::LossGrad)
-    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, true>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(LANES * kL), 0, st, a, vec_blocks);
+    launch_mode<A_, LANES, In, true>(a, st, static_cast<unsigned>(blocks), vec_tiles);
   else
-    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, false>), dim3(static_cast<unsigned>(blocks)),
-                       dim3(LANES * kL), 0, st, a, vec_blocks);
+    launch_mode<A_, LANES, In, false>(a, st, static_cast<unsigned>(blocks), vec_tiles);
   return hipGetLastError();
 }
 
@@ -398,8 +477,9 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
 
 bool tiled_supported(const StepArgs& a, LogitsType) { return a.A == 9 || a.A == 18; }
 
-// Lanes per workgroup: the count whose [t, b0:b0+LANES, :] run of logits is
-// 1152 bytes (nine 128-byte lines).
+// Lanes per workgroup: fp32 logits use the count whose [t, b0:b0+LANES, :] run
+// is 1152 bytes (nine 128-byte lines); bf16 logits keep 512-thread workgroups
+// (576- and 1152-byte runs), whose register budget avoids spills.
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups) {
   if (lt == LogitsType::F32) {
@@ -407,7 +487,7 @@ hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t
     if (a.A == 9) return launch_shape<9, 32, float>(a, mode, st, num_workgroups);
   } else {
     if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups);
-    if (a.A == 9) return launch_shape<9, 64, uint16_t>(a, mode, st, num_workgroups);
+    if (a.A == 9) return launch_shape<9, 32, uint16_t>(a, mode, st, num_workgroups);
   }
   return hipErrorNotSupported;
 }

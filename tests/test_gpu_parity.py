@@ -252,20 +252,25 @@ def test_gradient_invariants():
     assert np.all(np_out(out1.d_logits) == 0.0)
 
 
-def test_kernels_agree(monkeypatch):
-    """The tiled kernel and the generic lane-serial kernel give the same results."""
+@pytest.mark.parametrize("pidx", [0, 1])
+def test_kernels_agree(monkeypatch, pidx):
+    """The tiled kernel and the generic lane-serial kernel give the same results:
+    tightly where every weight is at most 1 (nothing amplifies rounding), to the
+    oracle's tolerance where the weights are unclipped."""
+    p = PARAM_SETS[4][pidx]
+    tight = pidx == 0
     for (T, B, A, bf16) in [(100, 4096, 9, False), (60, 1000, 18, False), (50, 777, 9, True)]:
         tr = make_random(T, B, A, 31 + A, noise_std=1.0, bf16=bf16)
         dev = to_device(tr)
-        p = PARAM_SETS[4][1]
-        log_case(f"kernel agreement T={T} B={B} A={A} bf16={bf16}")
+        log_case(f"kernel agreement T={T} B={B} A={A} bf16={bf16} {p.label()}")
         a = run_loss_grad(dev, p)
         monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
         b = run_loss_grad(dev, p)
         monkeypatch.delenv("VTRACE_KERNEL")
         for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+            kw = dict(rtol=2e-5, atol=2e-6) if tight else {}
             assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
-                         np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
+                         np_out(getattr(b, name)), **kw)
         # loss sums cancel (advantages of both signs): the oracle's tolerance
         for name in ("lane_losses", "losses"):
             assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
