@@ -73,10 +73,20 @@ def calibrate_copy(mib, reps):
     e1.record()
     torch.cuda.synchronize()
     read_ms = e0.elapsed_time(e1) / reps
+    # two reads and one write per element: the traffic mix of the V-trace step
+    other = torch.ones_like(src)
+    torch.add(src, other, out=dst)
+    e0.record()
+    for _ in range(reps):
+        torch.add(src, other, out=dst)
+    e1.record()
+    torch.cuda.synchronize()
+    mix_ms = e0.elapsed_time(e1) / reps
     print(json.dumps({"calibrate_copy_bytes_read": n * 4, "calibrate_copy_bytes_written": n * 4,
                       "copies": reps + 1, "copy_ms": copy_ms,
                       "copy_GBps_read_plus_write": 2 * n * 4 / copy_ms / 1e6,
-                      "sum_read_GBps": n * 4 / read_ms / 1e6}), flush=True)
+                      "sum_read_GBps": n * 4 / read_ms / 1e6,
+                      "add_2read_1write_GBps": 3 * n * 4 / mix_ms / 1e6}), flush=True)
 
 
 def kernel_source_digest() -> str:
@@ -128,22 +138,32 @@ def stored_traffic(avg_kernel_ms):
 
 
 def cpu_baseline(tr, p, target_s):
-    """The fp64 oracle on a bounded sample of lanes (all T), on one host thread."""
+    """The fp64 oracle, as it stands, on a bounded sample of lanes (all T), on one
+    host thread.  Lanes are independent, so the sample is run in chunks of at
+    most 2048 lanes to bound host memory; the reported time is their sum."""
     import numpy as np
     import oracle
     from synth import subset_lanes
 
     def run(n):
-        sub = subset_lanes(tr, np.arange(n))
-        t0 = time.perf_counter()
-        oracle.loss_and_grads(sub.target_logits, sub.behaviour_logits, sub.actions, sub.rewards,
-                              sub.discounts, sub.values, sub.bootstrap_value, p.rho_bar, p.c_bar,
-                              p.lam, p.baseline_cost, p.entropy_cost)
-        return time.perf_counter() - t0
+        wall = 0.0
+        for l0 in range(0, n, 2048):
+            sub = subset_lanes(tr, np.arange(l0, min(n, l0 + 2048)))
+            t0 = time.perf_counter()
+            oracle.loss_and_grads(sub.target_logits, sub.behaviour_logits, sub.actions,
+                                  sub.rewards, sub.discounts, sub.values, sub.bootstrap_value,
+                                  p.rho_bar, p.c_bar, p.lam, p.baseline_cost, p.entropy_cost)
+            wall += time.perf_counter() - t0
+        return wall
 
-    n0 = min(tr.B, 64)
-    t0 = run(n0)
-    n = int(min(tr.B, max(n0, n0 * target_s / max(t0, 1e-6))))
+    # Grow the sample until it costs a noticeable share of the target, then
+    # scale it to about target_s.
+    n = min(tr.B, 64)
+    t = run(n)
+    while t < target_s / 16 and n < tr.B:
+        n = min(tr.B, n * 4)
+        t = run(n)
+    n = int(min(tr.B, max(n, n * target_s / max(t, 1e-6))))
     wall = run(n)
     cpu_model = platform.processor()
     try:
@@ -159,8 +179,8 @@ def cpu_baseline(tr, p, target_s):
         "unit": "steps/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"{n} of {tr.B} lanes x all T={tr.T} steps ({tr.T * n} steps), "
-                  f"fp64 NumPy, one thread, {wall:.1f} s wall",
+        "sample": f"{n} of {tr.B} lanes x all T={tr.T} steps ({tr.T * n} steps) of the same "
+                  f"batch, fp64 NumPy oracle, one thread, {wall:.1f} s wall",
         "cpu_model": cpu_model,
         "host_cpus": os.cpu_count(),
     }
