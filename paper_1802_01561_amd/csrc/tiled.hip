@@ -76,6 +76,32 @@ __device__ __forceinline__ float exp_fast(float x) {
   return __builtin_amdgcn_exp2f(x * kLog2e);
 }
 
+// e^x in float64 for finite x <= 0: Cody-Waite reduction x = k ln2 + r with
+// |r| <= ln2/2 (ln2 split into a 32-bit head, so k*head is exact, and a tail),
+// then the Taylor series of e^r to degree 9 (truncation below 7e-12 relative)
+// and a scaling by 2^k.  Arguments below -1000 are raised to -1000, where the
+// result has already underflowed to zero; NaN stays NaN.
+__device__ __forceinline__ double exp_nonpos_f64(double x) {
+  constexpr double kLog2e = 1.4426950408889634;
+  constexpr double kLn2Hi = 0.6931471803691238;      // ln2 rounded to 32 bits
+  constexpr double kLn2Lo = 1.9082149292705877e-10;  // ln2 - kLn2Hi
+  x = x < -1000.0 ? -1000.0 : x;
+  const double k = __builtin_rint(x * kLog2e);
+  double r = fma(-k, kLn2Hi, x);
+  r = fma(-k, kLn2Lo, r);
+  double p = 2.7557319223985893e-06;  // 1/9!
+  p = fma(p, r, 2.48015873015873e-05);
+  p = fma(p, r, 0.0001984126984126984);
+  p = fma(p, r, 0.001388888888888889);
+  p = fma(p, r, 0.008333333333333333);
+  p = fma(p, r, 0.041666666666666664);
+  p = fma(p, r, 0.16666666666666666);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  return __builtin_ldexp(p, static_cast<int>(k));
+}
+
 template <int A_, int LANES, typename In>
 struct Tile {
   static constexpr int A = A_;
@@ -142,18 +168,18 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
 #pragma unroll
     for (int j = 0; j < A_; ++j) {
       const double d = static_cast<double>(logit_to_float(zr[j])) - static_cast<double>(mz);
-      const double x = exp(d);
+      const double x = exp_nonpos_f64(d);
       sz += x;
       e[j] = static_cast<float>(x);
       ed = fmaf(e[j], static_cast<float>(d), ed);
     }
 #pragma unroll
     for (int j = 0; j < A_; ++j)
-      sy += exp(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
+      sy += exp_nonpos_f64(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
     const double inv = 1.0 / sz;
     const double dza = static_cast<double>(za) - static_cast<double>(mz);
     const double dya = static_cast<double>(ya) - static_cast<double>(my);
-    const double ea = exp(dza);
+    const double ea = exp_nonpos_f64(dza);
     st.ratio = act_ok ? exp(dza - dya) * (sy * inv) : NAN;
     st.inv_s = static_cast<float>(inv);
     st.log_s = static_cast<float>(log(sz));
