@@ -23,6 +23,18 @@ Readings where the paper is silent (each is also listed in the design notes):
     value direction scaled by c_v; entropy loss c_e * sum_a pi log pi, whose
     negative gradient is the paper's entropy-bonus direction;
   * rho, c, v_s and the advantages are targets: no gradient flows through them.
+
+Correction variants (Sec. 5.2.3) and the alternative advantage of App. E.3 are
+selected by ``correction`` and ``q_estimate``:
+  * "vtrace": V-trace as above (the default);
+  * "none": no off-policy correction: rho = c = 1 in the value target and no
+    weight on the advantage; lambda still scales the trace, c_t = lambda;
+  * "epsilon": as "none", and the policy-gradient term uses log(pi(a) + eps)
+    instead of log pi(a) (eps = 1e-6 in the paper);
+  * "one_step_is": value target without correction (as "none"), advantage
+    multiplied by the truncated weight rho_s;
+  * q_estimate "vtrace": q_s = r_s + gamma_s v_{s+1};
+    q_estimate "baseline": q_s = r_s + gamma_s V(x_{s+1}).
 """
 
 from __future__ import annotations
@@ -30,6 +42,9 @@ from __future__ import annotations
 from typing import NamedTuple
 
 import numpy as np
+
+CORRECTIONS = ("vtrace", "none", "epsilon", "one_step_is")
+Q_ESTIMATES = ("vtrace", "baseline")
 
 
 def _f64(x):
@@ -116,10 +131,16 @@ def vtrace_targets_direct_sum(values, deltas, discounts, c):
     return vs
 
 
-def pg_advantages(rho, rewards, discounts, values, vs, bootstrap_value):
-    """rho_s (q_s - V(x_s)) with q_s = r_s + gamma_s v_{s+1} and v_T = V(x_T)   (Sec. 4.2)."""
-    vs_next = np.concatenate([_f64(vs)[1:], _f64(bootstrap_value)[None]], axis=0)
-    q = _f64(rewards) + _f64(discounts) * vs_next
+def pg_advantages(rho, rewards, discounts, values, vs, bootstrap_value, q_estimate="vtrace"):
+    """rho_s (q_s - V(x_s)) with q_s = r_s + gamma_s v_{s+1} and v_T = V(x_T)   (Sec. 4.2);
+    with q_estimate="baseline", q_s = r_s + gamma_s V(x_{s+1})   (App. E.3)."""
+    if q_estimate == "vtrace":
+        nxt = np.concatenate([_f64(vs)[1:], _f64(bootstrap_value)[None]], axis=0)
+    elif q_estimate == "baseline":
+        nxt = _values_next(values, bootstrap_value)
+    else:
+        raise ValueError(q_estimate)
+    q = _f64(rewards) + _f64(discounts) * nxt
     return _f64(rho) * (q - _f64(values))
 
 
@@ -134,16 +155,28 @@ class VtraceOut(NamedTuple):
 
 
 def vtrace(target_logits, behaviour_logits, actions, rewards, discounts, values,
-           bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, direct_sum=False) -> VtraceOut:
-    """V-trace targets v_s and policy-gradient advantages for a [T, B] batch."""
+           bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, direct_sum=False,
+           correction="vtrace", q_estimate="vtrace") -> VtraceOut:
+    """V-trace targets v_s and policy-gradient advantages for a [T, B] batch.
+
+    ``rho`` and ``c`` in the result are always the truncated weights; which of
+    them enter the value target and the advantage depends on ``correction``."""
+    if correction not in CORRECTIONS:
+        raise ValueError(correction)
     log_pi_a, log_mu_a, rho, c = truncated_is_weights(
         target_logits, behaviour_logits, actions, rho_bar, c_bar, lam)
-    deltas = temporal_differences(rho, rewards, discounts, values, bootstrap_value)
-    if direct_sum:
-        vs = vtrace_targets_direct_sum(values, deltas, discounts, c)
+    if correction == "vtrace":
+        rho_value, c_value, rho_pg = rho, c, rho
     else:
-        vs = vtrace_targets_recursive(values, bootstrap_value, deltas, discounts, c)
-    adv = pg_advantages(rho, rewards, discounts, values, vs, bootstrap_value)
+        ones = np.ones_like(rho)
+        rho_value, c_value = ones, np.float64(lam) * ones
+        rho_pg = rho if correction == "one_step_is" else ones
+    deltas = temporal_differences(rho_value, rewards, discounts, values, bootstrap_value)
+    if direct_sum:
+        vs = vtrace_targets_direct_sum(values, deltas, discounts, c_value)
+    else:
+        vs = vtrace_targets_recursive(values, bootstrap_value, deltas, discounts, c_value)
+    adv = pg_advantages(rho_pg, rewards, discounts, values, vs, bootstrap_value, q_estimate)
     return VtraceOut(log_pi_a, log_mu_a, rho, c, deltas, vs, adv)
 
 
@@ -156,11 +189,18 @@ class LossGradOut(NamedTuple):
     pg_advantages: np.ndarray
 
 
+def _pg_log_prob(log_pi_a, correction, epsilon):
+    """log pi(a|x) in the policy-gradient term; log(pi(a|x) + eps) for "epsilon"."""
+    if correction == "epsilon":
+        return np.log(np.exp(log_pi_a) + np.float64(epsilon))
+    return log_pi_a
+
+
 def total_loss_frozen_targets(target_logits, values, actions, pg_adv, vs,
-                              baseline_cost, entropy_cost):
+                              baseline_cost, entropy_cost, correction="vtrace", epsilon=1e-6):
     """Sum over batch and time of the three losses, with the targets held fixed.
 
-    policy gradient: -pg_adv_s * log pi(a_s|x_s)
+    policy gradient: -pg_adv_s * log pi(a_s|x_s)   (log(pi + eps) for "epsilon")
     baseline:        baseline_cost * 1/2 * (v_s - V(x_s))^2
     entropy:         entropy_cost * sum_a pi(a|x_s) log pi(a|x_s)
     """
@@ -168,7 +208,7 @@ def total_loss_frozen_targets(target_logits, values, actions, pg_adv, vs,
     a = np.asarray(actions, dtype=np.int64)[..., None]
     log_pi_a = np.take_along_axis(log_pi, a, axis=-1)[..., 0]
     pi = np.exp(log_pi)
-    pg = -np.sum(_f64(pg_adv) * log_pi_a)
+    pg = -np.sum(_f64(pg_adv) * _pg_log_prob(log_pi_a, correction, epsilon))
     base = np.float64(baseline_cost) * 0.5 * np.sum((_f64(vs) - _f64(values)) ** 2)
     ent = np.float64(entropy_cost) * np.sum(pi * log_pi)
     return pg + base + ent
@@ -176,30 +216,37 @@ def total_loss_frozen_targets(target_logits, values, actions, pg_adv, vs,
 
 def loss_and_grads(target_logits, behaviour_logits, actions, rewards, discounts, values,
                    bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0,
-                   baseline_cost=0.5, entropy_cost=0.01) -> LossGradOut:
+                   baseline_cost=0.5, entropy_cost=0.01, *, correction="vtrace",
+                   q_estimate="vtrace", epsilon=1e-6) -> LossGradOut:
     """The three losses of the V-trace actor-critic update (Sec. 4.2) and their
     gradients with respect to the target logits and the values."""
     vt = vtrace(target_logits, behaviour_logits, actions, rewards, discounts, values,
-                bootstrap_value, rho_bar, c_bar, lam)
+                bootstrap_value, rho_bar, c_bar, lam, correction=correction,
+                q_estimate=q_estimate)
     c_v = np.float64(baseline_cost)
     c_e = np.float64(entropy_cost)
     log_pi = log_softmax(target_logits)
     pi = np.exp(log_pi)
     neg_entropy = np.sum(pi * log_pi, axis=-1)  # sum_a pi log pi = -H
 
-    pg_tb = -vt.pg_advantages * vt.log_pi_a
+    pg_tb = -vt.pg_advantages * _pg_log_prob(vt.log_pi_a, correction, epsilon)
     base_tb = c_v * 0.5 * (vt.vs - _f64(values)) ** 2
     ent_tb = c_e * neg_entropy
     lane = np.stack([pg_tb.sum(axis=0), base_tb.sum(axis=0), ent_tb.sum(axis=0)], axis=-1)
     pg_l, base_l, ent_l = pg_tb.sum(), base_tb.sum(), ent_tb.sum()
     losses = np.array([pg_l + base_l + ent_l, pg_l, base_l, ent_l], dtype=np.float64)
 
-    # d/dz_j of -adv*log pi_a is adv*(pi_j - 1[j = a]);
+    # d/dz_j of -adv*log pi_a is adv*(pi_j - 1[j = a]); of -adv*log(pi_a + eps)
+    # it is adv*w*(pi_j - 1[j = a]) with w = pi_a/(pi_a + eps);
     # d/dz_j of sum_k pi_k log pi_k is pi_j*(log pi_j + H).
     onehot = np.zeros_like(pi)
     np.put_along_axis(onehot, np.asarray(actions, dtype=np.int64)[..., None], 1.0, axis=-1)
     entropy = -neg_entropy
-    d_logits = (vt.pg_advantages[..., None] * (pi - onehot)
+    w = np.ones_like(vt.pg_advantages)
+    if correction == "epsilon":
+        pi_a = np.exp(vt.log_pi_a)
+        w = pi_a / (pi_a + np.float64(epsilon))
+    d_logits = ((vt.pg_advantages * w)[..., None] * (pi - onehot)
                 + c_e * pi * (log_pi + entropy[..., None]))
     d_values = c_v * (_f64(values) - vt.vs)
     return LossGradOut(losses, lane, d_logits, d_values, vt.vs, vt.pg_advantages)

@@ -423,22 +423,17 @@ def _mutant(replacements):
 
 MUTATIONS = {
     "trace_drops_c": [("_f64(discounts[s]) * c[s] * (vs", "_f64(discounts[s]) * (vs")],
-    "trace_uses_rho": [("deltas = temporal_differences(rho, rewards, discounts, values, bootstrap_value)\n"
-                        "    if direct_sum:\n        vs = vtrace_targets_direct_sum(values, deltas, discounts, c)\n"
-                        "    else:\n        vs = vtrace_targets_recursive(values, bootstrap_value, deltas, discounts, c)",
-                        "deltas = temporal_differences(rho, rewards, discounts, values, bootstrap_value)\n"
-                        "    if direct_sum:\n        vs = vtrace_targets_direct_sum(values, deltas, discounts, rho)\n"
-                        "    else:\n        vs = vtrace_targets_recursive(values, bootstrap_value, deltas, discounts, rho)")],
+    "trace_uses_rho": [("rho_value, c_value, rho_pg = rho, c, rho", "rho_value, c_value, rho_pg = rho, rho, rho")],
     "delta_uses_V_t": [("_f64(discounts) * _values_next(values, bootstrap_value)", "_f64(discounts) * _f64(values)")],
     "delta_sign": [("\n                        - _f64(values))", "\n                        + _f64(values))")],
     "lambda_scales_rho": [("rho = np.minimum(np.float64(rho_bar), ratio)",
                            "rho = np.float64(lam) * np.minimum(np.float64(rho_bar), ratio)")],
     "min_swapped_bars": [("rho = np.minimum(np.float64(rho_bar), ratio)", "rho = np.minimum(np.float64(c_bar), ratio)")],
     "ratio_inverted": [("ratio = np.exp(log_pi_a - log_mu_a)", "ratio = np.exp(log_mu_a - log_pi_a)")],
-    "pg_uses_v_s": [("vs_next = np.concatenate([_f64(vs)[1:], _f64(bootstrap_value)[None]], axis=0)",
-                     "vs_next = _f64(vs)")],
+    "pg_uses_v_s": [("nxt = np.concatenate([_f64(vs)[1:], _f64(bootstrap_value)[None]], axis=0)",
+                     "nxt = _f64(vs)")],
     "pg_drops_rho": [("return _f64(rho) * (q - _f64(values))", "return (q - _f64(values))")],
-    "pg_drops_discount": [("q = _f64(rewards) + _f64(discounts) * vs_next", "q = _f64(rewards) + vs_next")],
+    "pg_drops_discount": [("q = _f64(rewards) + _f64(discounts) * nxt", "q = _f64(rewards) + nxt")],
     "recursion_wrong_V": [("(vs[s + 1] - V_ext[s + 1])", "(vs[s + 1] - V_ext[s])")],
     "grad_entropy_sign": [("+ c_e * pi * (log_pi + entropy[..., None]))", "- c_e * pi * (log_pi + entropy[..., None]))")],
     "grad_onehot_shift": [("np.asarray(actions, dtype=np.int64)[..., None], 1.0, axis=-1)",
