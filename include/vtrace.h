@@ -81,6 +81,32 @@ typedef enum {
   VTRACE_BF16 = 1  /* bfloat16 logits (upper half of a binary32) */
 } vtrace_dtype;
 
+/*
+ * Off-policy correction variants compared in the paper (Sec. 5.2.3) and the
+ * choice of the Q estimate in the advantage (App. E.3).  The default, V-trace
+ * with q_s = r_s + gamma_s v_{s+1}, is what vtrace_targets and vtrace_loss_grad
+ * compute.
+ */
+typedef enum {
+  VTRACE_CORRECTION_VTRACE = 0,     /* V-trace (Sec. 4) */
+  VTRACE_CORRECTION_NONE = 1,       /* no correction: rho = c = 1 in the target (c = lambda with
+                                       lambda < 1), no weight on the advantage */
+  VTRACE_CORRECTION_EPSILON = 2,    /* as NONE, with log(pi(a|x) + epsilon) in place of
+                                       log pi(a|x) in the policy-gradient term */
+  VTRACE_CORRECTION_ONE_STEP_IS = 3 /* uncorrected target (as NONE), advantage times rho_s */
+} vtrace_correction;
+
+typedef enum {
+  VTRACE_Q_VTRACE = 0,  /* q_s = r_s + gamma_s v_{s+1} (Sec. 4.2) */
+  VTRACE_Q_BASELINE = 1 /* q_s = r_s + gamma_s V(x_{s+1}) (App. E.3) */
+} vtrace_q_estimate;
+
+typedef struct {
+  int32_t correction; /* a vtrace_correction */
+  int32_t q_estimate; /* a vtrace_q_estimate */
+  float epsilon;      /* VTRACE_CORRECTION_EPSILON only: finite and > 0 (the paper uses 1e-6) */
+} vtrace_variant;
+
 /* Version of this interface; bumped on any incompatible change. */
 int vtrace_abi_version(void);
 
@@ -154,6 +180,31 @@ vtrace_status vtrace_loss_grad(
     const float* rewards, const float* discounts, const float* values,
     const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
     float baseline_cost, float entropy_cost,
+    float* losses, float* d_logits, float* d_values,
+    float* vs, float* pg_advantages, float* lane_losses,
+    void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
+
+/*
+ * vtrace_targets / vtrace_loss_grad with a correction variant.  `variant` is a
+ * HOST pointer read during the call (NULL = V-trace, the default); an unknown
+ * correction or Q estimate, or a bad epsilon, gives VTRACE_ERR_PARAM.  NONE and
+ * EPSILON do not use the importance ratio: behaviour_logits must still be a
+ * valid [T,B,A] array, but its values do not change the outputs.
+ */
+vtrace_status vtrace_targets_ex(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* values,
+    const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
+    const vtrace_variant* variant, float* vs, float* pg_advantages,
+    void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
+
+vtrace_status vtrace_loss_grad_ex(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* values,
+    const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
+    float baseline_cost, float entropy_cost, const vtrace_variant* variant,
     float* losses, float* d_logits, float* d_values,
     float* vs, float* pg_advantages, float* lane_losses,
     void* workspace, size_t workspace_bytes, vtrace_stream_t stream);

@@ -24,6 +24,16 @@ STATUS_NAMES = {
     7: "VTRACE_ERR_HIP",
 }
 
+CORRECTIONS = {"vtrace": 0, "none": 1, "epsilon": 2, "one_step_is": 3}
+Q_ESTIMATES = {"vtrace": 0, "baseline": 1}
+
+
+class Variant(ctypes.Structure):
+    """vtrace_variant: correction variant, Q estimate and epsilon."""
+    _fields_ = [("correction", ctypes.c_int32), ("q_estimate", ctypes.c_int32),
+                ("epsilon", ctypes.c_float)]
+
+
 # Every symbol include/vtrace.h declares, with (restype, argtypes).
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
@@ -38,6 +48,10 @@ SIGNATURES = {
     "vtrace_targets": (ctypes.c_int, _INPUTS + [_P, _P, _P, ctypes.c_size_t, _P]),
     "vtrace_loss_grad": (ctypes.c_int, _INPUTS + [_F, _F, _P, _P, _P, _P, _P, _P, _P,
                                                   ctypes.c_size_t, _P]),
+    "vtrace_targets_ex": (ctypes.c_int, _INPUTS + [ctypes.POINTER(Variant), _P, _P, _P,
+                                                   ctypes.c_size_t, _P]),
+    "vtrace_loss_grad_ex": (ctypes.c_int, _INPUTS + [_F, _F, ctypes.POINTER(Variant), _P, _P, _P,
+                                                     _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "vtrace_gather_logits": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _P, _P]),
     "vtrace_error_flag": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_int32), _P]),
 }

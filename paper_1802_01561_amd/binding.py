@@ -12,7 +12,7 @@ from typing import NamedTuple, Optional
 
 import torch
 
-from ._lib import VTRACE_BF16, VTRACE_F32, check, lib
+from ._lib import CORRECTIONS, Q_ESTIMATES, VTRACE_BF16, VTRACE_F32, Variant, check, lib
 
 __all__ = [
     "LossGrad",
@@ -74,6 +74,14 @@ def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values
     return T, B, A, code, dev
 
 
+def _variant(correction, q_estimate, epsilon):
+    """A vtrace_variant for the _ex entry points (Sec. 5.2.3, App. E.3)."""
+    try:
+        return Variant(CORRECTIONS[correction], Q_ESTIMATES[q_estimate], float(epsilon))
+    except KeyError as e:
+        raise ValueError(f"unknown correction or q_estimate: {e}") from None
+
+
 def vtrace_abi_version() -> int:
     return lib().vtrace_abi_version()
 
@@ -112,8 +120,13 @@ class LossGrad(NamedTuple):
 
 def vtrace_targets(target_logits, behaviour_logits, actions, rewards, discounts, values,
                    bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, vs=None,
-                   pg_advantages=None, workspace: Optional[Workspace] = None, stream=None):
-    """V-trace targets v_s and advantages; returns (vs, pg_advantages)."""
+                   pg_advantages=None, workspace: Optional[Workspace] = None, stream=None,
+                   correction="vtrace", q_estimate="vtrace", epsilon=1e-6):
+    """V-trace targets v_s and advantages; returns (vs, pg_advantages).
+
+    ``correction`` ("vtrace", "none", "epsilon", "one_step_is") and
+    ``q_estimate`` ("vtrace", "baseline") select the paper's variants."""
+    variant = _variant(correction, q_estimate, epsilon)
     T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
                                  values, bootstrap_value)
     if vs is None:
@@ -123,10 +136,10 @@ def vtrace_targets(target_logits, behaviour_logits, actions, rewards, discounts,
     _require(vs, "vs", (T, B), torch.float32, dev)
     _require(pg_advantages, "pg_advantages", (T, B), torch.float32, dev)
     ws, nws = (None, 0) if workspace is None else (_p(workspace.tensor), workspace.nbytes)
-    check(lib().vtrace_targets(
+    check(lib().vtrace_targets_ex(
         T, B, A, code, _p(target_logits), _p(behaviour_logits), _p(actions), _p(rewards),
         _p(discounts), _p(values), _p(bootstrap_value), rho_bar, c_bar, lam,
-        _p(vs), _p(pg_advantages), ws, nws, _stream(stream)))
+        ctypes.byref(variant), _p(vs), _p(pg_advantages), ws, nws, _stream(stream)))
     return vs, pg_advantages
 
 
@@ -134,11 +147,14 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
                      bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, baseline_cost=0.5,
                      entropy_cost=0.01, *, workspace: Optional[Workspace] = None,
                      with_vs=False, with_pg_advantages=False, with_lane_losses=False,
-                     out: Optional[LossGrad] = None, stream=None) -> LossGrad:
+                     out: Optional[LossGrad] = None, stream=None, correction="vtrace",
+                     q_estimate="vtrace", epsilon=1e-6) -> LossGrad:
     """Fused V-trace targets, losses and gradients w.r.t. logits and values.
 
     ``out`` may hold preallocated output tensors (fields left None are skipped
-    when optional, allocated when required)."""
+    when optional, allocated when required).  ``correction`` and ``q_estimate``
+    select the paper's variants, as in vtrace_targets."""
+    variant = _variant(correction, q_estimate, epsilon)
     T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
                                  values, bootstrap_value)
     if workspace is None:
@@ -159,10 +175,11 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
         _require(out.pg_advantages, "pg_advantages", (T, B), torch.float32, dev)
     if out.lane_losses is not None:
         _require(out.lane_losses, "lane_losses", (B, 3), torch.float32, dev)
-    check(lib().vtrace_loss_grad(
+    check(lib().vtrace_loss_grad_ex(
         T, B, A, code, _p(target_logits), _p(behaviour_logits), _p(actions), _p(rewards),
         _p(discounts), _p(values), _p(bootstrap_value), rho_bar, c_bar, lam,
-        baseline_cost, entropy_cost, _p(out.losses), _p(out.d_logits), _p(out.d_values),
+        baseline_cost, entropy_cost, ctypes.byref(variant), _p(out.losses), _p(out.d_logits),
+        _p(out.d_values),
         _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses),
         _p(workspace.tensor), workspace.nbytes, _stream(stream)))
     return out

@@ -96,6 +96,23 @@ void attach_workspace(StepArgs* a, void* ws) {
   a->partials = reinterpret_cast<double*>(base + vtrace::kWsHeaderBytes);
 }
 
+// Copies a caller's variant into the launch arguments (NULL = V-trace).
+vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
+  a->correction = VTRACE_CORRECTION_VTRACE;
+  a->q_estimate = VTRACE_Q_VTRACE;
+  a->epsilon = 0.0f;
+  if (v == nullptr) return VTRACE_OK;
+  if (v->correction < VTRACE_CORRECTION_VTRACE || v->correction > VTRACE_CORRECTION_ONE_STEP_IS)
+    return VTRACE_ERR_PARAM;
+  if (v->q_estimate != VTRACE_Q_VTRACE && v->q_estimate != VTRACE_Q_BASELINE) return VTRACE_ERR_PARAM;
+  if (v->correction == VTRACE_CORRECTION_EPSILON && !(std::isfinite(v->epsilon) && v->epsilon > 0.0f))
+    return VTRACE_ERR_PARAM;
+  a->correction = v->correction;
+  a->q_estimate = v->q_estimate;
+  a->epsilon = v->epsilon;
+  return VTRACE_OK;
+}
+
 vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s) {
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   int64_t nwg = 0;
@@ -121,7 +138,8 @@ const char* vtrace_status_string(vtrace_status s) {
     case VTRACE_ERR_DTYPE: return "unknown logits dtype";
     case VTRACE_ERR_PARAM:
       return "bad parameter: rho_bar, c_bar must be >= 0 (inf allowed), lambda in [0,1], "
-             "costs finite, none NaN";
+             "costs finite, none NaN; a variant needs a known correction and Q estimate and, "
+             "for epsilon-correction, a finite epsilon > 0";
     case VTRACE_ERR_ALIGN: return "misaligned pointer: logits/d_logits/gathered need 16 bytes, others 4";
     case VTRACE_ERR_WORKSPACE: return "workspace missing or smaller than vtrace_workspace_bytes()";
     case VTRACE_ERR_HIP: return "the HIP runtime rejected the kernel launch";
@@ -152,6 +170,19 @@ vtrace_status vtrace_targets(int64_t T, int64_t B, int64_t A, vtrace_dtype logit
                              const float* values, const float* bootstrap_value, float rho_bar,
                              float c_bar, float lambda, float* vs, float* pg_advantages,
                              void* workspace, size_t workspace_bytes, vtrace_stream_t stream) {
+  return vtrace_targets_ex(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
+                           rewards, discounts, values, bootstrap_value, rho_bar, c_bar, lambda,
+                           nullptr, vs, pg_advantages, workspace, workspace_bytes, stream);
+}
+
+vtrace_status vtrace_targets_ex(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                                const void* target_logits, const void* behaviour_logits,
+                                const int32_t* actions, const float* rewards,
+                                const float* discounts, const float* values,
+                                const float* bootstrap_value, float rho_bar, float c_bar,
+                                float lambda, const vtrace_variant* variant, float* vs,
+                                float* pg_advantages, void* workspace, size_t workspace_bytes,
+                                vtrace_stream_t stream) {
   LogitsType lt;
   vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
                                   rewards, discounts, values, bootstrap_value, rho_bar, c_bar,
@@ -163,6 +194,8 @@ vtrace_status vtrace_targets(int64_t T, int64_t B, int64_t A, vtrace_dtype logit
                          values, bootstrap_value, rho_bar, c_bar, lambda);
   a.vs = vs;
   a.pg_adv = pg_advantages;
+  st = apply_variant(variant, &a);
+  if (st != VTRACE_OK) return st;
   if (workspace) {
     if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
     if (workspace_bytes < vtrace::kWsHeaderBytes) return VTRACE_ERR_WORKSPACE;
@@ -182,6 +215,22 @@ vtrace_status vtrace_loss_grad(int64_t T, int64_t B, int64_t A, vtrace_dtype log
                                float* losses, float* d_logits, float* d_values, float* vs,
                                float* pg_advantages, float* lane_losses, void* workspace,
                                size_t workspace_bytes, vtrace_stream_t stream) {
+  return vtrace_loss_grad_ex(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
+                             rewards, discounts, values, bootstrap_value, rho_bar, c_bar, lambda,
+                             baseline_cost, entropy_cost, nullptr, losses, d_logits, d_values, vs,
+                             pg_advantages, lane_losses, workspace, workspace_bytes, stream);
+}
+
+vtrace_status vtrace_loss_grad_ex(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                                  const void* target_logits, const void* behaviour_logits,
+                                  const int32_t* actions, const float* rewards,
+                                  const float* discounts, const float* values,
+                                  const float* bootstrap_value, float rho_bar, float c_bar,
+                                  float lambda, float baseline_cost, float entropy_cost,
+                                  const vtrace_variant* variant, float* losses, float* d_logits,
+                                  float* d_values, float* vs, float* pg_advantages,
+                                  float* lane_losses, void* workspace, size_t workspace_bytes,
+                                  vtrace_stream_t stream) {
   LogitsType lt;
   vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
                                   rewards, discounts, values, bootstrap_value, rho_bar, c_bar,
@@ -206,6 +255,8 @@ vtrace_status vtrace_loss_grad(int64_t T, int64_t B, int64_t A, vtrace_dtype log
   a.vs = vs;
   a.pg_adv = pg_advantages;
   a.lane_losses = lane_losses;
+  st = apply_variant(variant, &a);
+  if (st != VTRACE_OK) return st;
   attach_workspace(&a, workspace);
   return launch(a, lt, Mode::LossGrad, as_hip(stream));
 }

@@ -32,6 +32,33 @@ __device__ __forceinline__ double importance_ratio(float za, float mz, float ya,
   return exp(dz - dy) * (s_mu / s_pi);
 }
 
+// Correction variants of Sec. 5.2.3 (values of StepArgs::correction).
+constexpr int kCorrVtrace = 0, kCorrNone = 1, kCorrEpsilon = 2, kCorrOneStepIs = 3;
+constexpr int kQBaseline = 1;  // StepArgs::q_estimate: q_s = r_s + gamma_s V(x_{s+1})
+
+// The weights a step contributes under a correction variant: rho and c in the
+// value target, and the weight on the advantage.  V-trace uses the truncated
+// rho_t and c_t everywhere; the uncorrected variants use rho = 1 and c = lambda
+// in the target, and one-step importance sampling weights the advantage by
+// rho_t.  A step with an invalid action gets NaN weights in every variant.
+struct StepWeights {
+  double rho_v, c_v, rho_pg;
+};
+__device__ __forceinline__ StepWeights variant_weights(int correction, double rho, double c,
+                                                       double lam, bool act_ok) {
+  StepWeights w;
+  if (correction == kCorrVtrace) {
+    w.rho_v = rho;
+    w.c_v = c;
+    w.rho_pg = rho;
+  } else {
+    w.rho_v = act_ok ? 1.0 : NAN;
+    w.c_v = act_ok ? lam : NAN;
+    w.rho_pg = correction == kCorrOneStepIs ? rho : w.rho_v;
+  }
+  return w;
+}
+
 // Butterfly sum over a wave.  Every lane ends with the same value, and the
 // order of additions is fixed, so the result is reproducible bit for bit.
 __device__ __forceinline__ double wave_sum(double v) {

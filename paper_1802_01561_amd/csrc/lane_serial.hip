@@ -63,14 +63,15 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
 
       const double ratio = valid ? importance_ratio(za, mz, ya, my, sz, sy) : NAN;
       if (!valid) raise_error_flag(a.error_flag);
-      const double rho = clip_above(ratio, rho_bar);
-      const double c = lam * clip_above(ratio, c_bar);
+      const StepWeights w = variant_weights(a.correction, clip_above(ratio, rho_bar),
+                                            lam * clip_above(ratio, c_bar), lam, valid);
 
       const double r = a.rewards[idx], g = a.discounts[idx], V = a.values[idx];
-      const double delta = rho * (r + g * V_next - V);
-      const double A_t = delta + g * c * A_next;  // v_t - V(x_t)
+      const double delta = w.rho_v * (r + g * V_next - V);
+      const double A_t = delta + g * w.c_v * A_next;  // v_t - V(x_t)
       const double v_t = V + A_t;
-      const double adv = rho * (r + g * v_next - V);
+      const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+      const double adv = w.rho_pg * (r + g * q_next - V);
 
       if (a.vs) a.vs[idx] = static_cast<float>(v_t);
       if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
@@ -83,7 +84,11 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
         const float H = log_s - ed * inv;
         // 1 - pi(a): the other actions' mass, without cancellation.
         const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) / sz);
-        const float adv32 = valid ? static_cast<float>(adv) : NAN;
+        // epsilon-correction: -adv log(pi_a + eps) has gradient adv pi_a/(pi_a + eps) (pi_j - 1[j=a]).
+        const float pa = ea * inv;
+        const bool eps_mode = a.correction == kCorrEpsilon;
+        const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
+        const float adv32 = valid ? static_cast<float>(adv) * pg_w : NAN;
         float* dl = a.d_logits + idx * A;
         for (int64_t j = 0; j < A; ++j) {
           const float dz = logit_to_float(zr[j]) - mz;
@@ -91,7 +96,9 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
           const float pg_term = (j == act) ? -one_minus_pa : p;
           dl[j] = adv32 * pg_term + ce * p * ((dz - log_s) + H);
         }
-        const double log_pa = valid ? static_cast<double>(za - mz) - static_cast<double>(log_s) : NAN;
+        const double log_pa = !valid ? NAN
+                              : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
+                                         : static_cast<double>(za - mz) - static_cast<double>(log_s);
         acc_pg += -adv * log_pa;
         acc_base += 0.5 * (v_t - V) * (v_t - V);
         acc_ent += -static_cast<double>(H);

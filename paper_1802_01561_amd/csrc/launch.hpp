@@ -20,6 +20,10 @@ struct StepArgs {
   const float* bootstrap_value;  // [B]
   float rho_bar, c_bar, lambda;
   float baseline_cost, entropy_cost;
+  // Correction variant (0 = V-trace, 1 = none, 2 = epsilon, 3 = one-step IS),
+  // Q estimate (0: r + gamma v_{s+1}, 1: r + gamma V(x_{s+1})) and epsilon.
+  int correction, q_estimate;
+  float epsilon;
   // outputs (any may be null except where a kernel variant requires them)
   float* losses;       // [4]
   float* d_logits;     // [T,B,A]

@@ -328,18 +328,18 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     if (!act_ok) raise_error_flag(a.error_flag);
     float e[A_];
     const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, e);
-    const double rho = clip_above(st.ratio, rho_bar);
-    const double c = lam * clip_above(st.ratio, c_bar);
+    const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
+                                          lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
     const double r = r32, g = g32, V = V32;
     double V_next = dpp_f64<kRowShl1>(V);
     if (s == kL - 1) V_next = cy.V;
-    const double delta = rho * (r + g * V_next - V);
+    const double delta = w.rho_v * (r + g * V_next - V);
 
     // Suffix scan over the row.  Step 15 first absorbs the carry from the later
     // chunk, so that after the scan D holds v_t - V(x_t) on every thread:
     // (G, D) composes the maps of steps s..15 applied to that carry.
-    double G = g * c, D = delta;
+    double G = g * w.c_v, D = delta;
     if (s == kL - 1) D = fma(G, cy.A, D);
     static_for<4>([&](auto I) {
       constexpr int off = 1 << decltype(I)::value;
@@ -354,7 +354,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const double v_t = V + A_t;
     double v_next = dpp_f64<kRowShl1>(v_t);
     if (s == kL - 1) v_next = cy.v;
-    const double adv = rho * (r + g * v_next - V);
+    const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+    const double adv = w.rho_pg * (r + g * q_next - V);
 
     // The row's first step becomes the carry of the earlier chunk, held by the
     // row's last thread, the only one that reads it.
@@ -371,16 +372,22 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       // d_logits_j = adv (pi_j - 1[j=a]) + ce pi_j (log pi_j + H), where
       // log pi_j + H = z_j - K.  For j != a this is e_j (alpha + beta z_j).
       const float K = st.mz + st.log_s - st.H;
-      const float adv32 = static_cast<float>(adv);
+      // epsilon-correction: the policy-gradient term is -adv log(pi_a + eps),
+      // whose gradient is adv pi_a/(pi_a + eps) (pi_j - 1[j=a]).
+      const float pa = st.e_a * st.inv_s;
+      const bool eps_mode = a.correction == kCorrEpsilon;
+      const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
+      const float adv32 = static_cast<float>(adv) * pg_w;
       const float beta = st.inv_s * ce;
       const float alpha = st.inv_s * adv32 - beta * K;
       const float za = logit_to_float(zr[act_c]);
-      const float out_a =
-          -adv32 * st.one_minus_pa + ce * (st.e_a * st.inv_s) * (za - K);
+      const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
       if (step_ok) {
         a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
         const double log_pa =
-            act_ok ? static_cast<double>(za - st.mz) - static_cast<double>(st.log_s) : NAN;
+            !act_ok ? NAN
+            : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
+                       : static_cast<double>(za - st.mz) - static_cast<double>(st.log_s);
         cy.pg += -adv * log_pa;
         cy.base += 0.5 * A_t * A_t;
         cy.ent += -static_cast<double>(st.H);
@@ -473,8 +480,10 @@ __global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t nu
 
 template <int A_, int LANES, typename In, bool kGrad>
 void launch_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int64_t vec_tiles) {
-  // float32 ratios suffice when no weight can exceed 1.
-  const bool precise = !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+  // float32 ratios suffice unless V-trace's weights can exceed 1 (products of c
+  // can then grow and amplify rounding).  The other variants use the ratio, if
+  // at all, only as one factor of one step's advantage.
+  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
   if (precise)
     hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, true>), dim3(blocks), dim3(LANES * kL),
                        0, st, a, vec_tiles);

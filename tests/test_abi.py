@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 9
+    assert len(names) == 11
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(_lib.SIGNATURES)
@@ -125,6 +125,46 @@ def test_loss_grad_rejects_outputs_and_workspace(L):
     assert _loss(L, nws=16) == WS
     assert _loss(L, B=4096, nws=L.vtrace_workspace_bytes(5, 4096, 9) - 1) == WS
     assert _loss(L, ws=P + 8) == ALIGN
+
+
+def test_variant_validation(L):
+    V = _lib.Variant
+    base = dict(T=5, B=4, A=9, dt=0, tl=P, bl=P, act=P, r=P, d=P, v=P, boot=P)
+
+    def loss_ex(variant, **kw):
+        a = dict(base, rho=1.0, c=1.0, lam=1.0, cv=0.5, ce=0.01, losses=P, dl=P, dv=P, ws=P,
+                 nws=1 << 20)
+        a.update(kw)
+        return L.vtrace_loss_grad_ex(a["T"], a["B"], a["A"], a["dt"], a["tl"], a["bl"], a["act"],
+                                     a["r"], a["d"], a["v"], a["boot"], a["rho"], a["c"], a["lam"],
+                                     a["cv"], a["ce"], variant, a["losses"], a["dl"], a["dv"], None,
+                                     None, None, a["ws"], a["nws"], None)
+
+    def targets_ex(variant, **kw):
+        a = dict(base, rho=1.0, c=1.0, lam=1.0)
+        a.update(kw)
+        return L.vtrace_targets_ex(a["T"], a["B"], a["A"], a["dt"], a["tl"], a["bl"], a["act"],
+                                   a["r"], a["d"], a["v"], a["boot"], a["rho"], a["c"], a["lam"],
+                                   variant, P, P, None, 0, None)
+
+    for bad in (V(4, 0, 1e-6), V(-1, 0, 1e-6), V(0, 2, 1e-6), V(0, -1, 1e-6), V(2, 0, 0.0),
+                V(2, 0, -1e-6), V(2, 0, math.nan), V(2, 0, math.inf)):
+        assert loss_ex(ctypes.byref(bad)) == PARAM
+        assert targets_ex(ctypes.byref(bad)) == PARAM
+    # a valid variant with another invalid argument is still rejected before launch
+    for good in (None, ctypes.byref(V(0, 0, 0.0)), ctypes.byref(V(3, 1, 0.0)),
+                 ctypes.byref(V(2, 0, 1e-6))):
+        assert loss_ex(good, T=0) == SHAPE
+        assert loss_ex(good, ws=None) == WS
+        assert targets_ex(good, lam=2.0) == PARAM
+
+
+def test_python_variant_names():
+    from paper_1802_01561_amd import binding
+    assert binding._variant("one_step_is", "baseline", 1e-6).correction == 3
+    assert binding._variant("epsilon", "vtrace", 1e-6).q_estimate == 0
+    with pytest.raises(ValueError):
+        binding._variant("retrace", "vtrace", 1e-6)
 
 
 def test_gather_and_flag_reject(L):

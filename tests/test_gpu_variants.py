@@ -1,0 +1,100 @@
+"""GPU parity of the correction variants (Sec. 5.2.3) and the baseline Q
+estimate (App. E.3) against the oracle, through the _ex entry points."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1802_01561_amd as vt
+from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from synth import Params, make_config, make_random
+
+pytestmark = pytest.mark.gpu
+
+CORRECTIONS = ["vtrace", "none", "epsilon", "one_step_is"]
+Q_ESTIMATES = ["vtrace", "baseline"]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def check_variant(tr, p, correction, q_estimate, epsilon=1e-6):
+    dev = to_device(tr)
+    out = vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                              baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
+                              with_vs=True, with_pg_advantages=True, with_lane_losses=True,
+                              correction=correction, q_estimate=q_estimate, epsilon=epsilon)
+    vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                               correction=correction, q_estimate=q_estimate, epsilon=epsilon)
+    torch.cuda.synchronize()
+    o = oracle.loss_and_grads(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
+                              p.entropy_cost, correction=correction, q_estimate=q_estimate,
+                              epsilon=epsilon)
+    tag = f"{correction}/{q_estimate}"
+    assert_close(f"{tag} vs", np_out(out.vs), o.vs)
+    assert_close(f"{tag} pg_advantages", np_out(out.pg_advantages), o.pg_advantages)
+    assert_close(f"{tag} d_values", np_out(out.d_values), o.d_values)
+    assert_close(f"{tag} d_logits", np_out(out.d_logits), o.d_logits)
+    assert_close(f"{tag} lane_losses", np_out(out.lane_losses), o.lane_losses)
+    assert_close(f"{tag} losses", np_out(out.losses), o.losses)
+    assert_close(f"{tag} targets.vs", np_out(vs), o.vs)
+    assert_close(f"{tag} targets.pg_advantages", np_out(pg), o.pg_advantages)
+
+
+@pytest.mark.parametrize("correction", CORRECTIONS)
+@pytest.mark.parametrize("q_estimate", Q_ESTIMATES)
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_variants_on_configs(cfg, correction, q_estimate):
+    tr = make_config(cfg)
+    for p in (Params(1.0, 1.0, 1.0), Params(2.0, 1.0, 0.9), Params(math.inf, math.inf, 1.0)):
+        log_case(f"config {cfg} {correction}/{q_estimate} {p.label()}")
+        check_variant(tr, p, correction, q_estimate)
+
+
+@pytest.mark.parametrize("correction", CORRECTIONS)
+@pytest.mark.parametrize("shape", [(37, 45, 18), (33, 70, 9), (12, 10, 7)])
+@pytest.mark.parametrize("bf16", [False, True])
+def test_variants_ragged_and_generic(correction, shape, bf16):
+    T, B, A = shape
+    tr = make_random(T, B, A, 90 + T + B + A, noise_std=1.0, bf16=bf16)
+    log_case(f"variant {correction} T={T} B={B} A={A} bf16={bf16}")
+    check_variant(tr, Params(1.0, 0.5, 0.95), correction, "baseline")
+    check_variant(tr, Params(1.0, 1.0, 1.0), correction, "vtrace")
+
+
+def test_epsilon_correction_with_unlikely_actions():
+    """Taken actions with pi(a) near epsilon, where the correction changes the result."""
+    tr = make_random(40, 64, 18, 5, noise_std=1.5)
+    tr.target_logits[..., 3] -= np.float32(13.0)
+    tr.actions[::3] = 3
+    for eps in (1e-6, 1e-3):
+        log_case(f"epsilon-correction eps={eps}")
+        check_variant(tr, Params(1.0, 1.0, 1.0), "epsilon", "vtrace", epsilon=eps)
+    # the correction is visible: the gradient differs from no-correction's
+    dev = to_device(tr)
+    a = vt.vtrace_loss_grad(**dev, correction="epsilon", epsilon=1e-3)
+    b = vt.vtrace_loss_grad(**dev, correction="none")
+    torch.cuda.synchronize()
+    assert not np.allclose(np_out(a.d_logits), np_out(b.d_logits))
+
+
+def test_variant_kernels_agree(monkeypatch):
+    tr = make_random(64, 300, 9, 17, noise_std=1.0)
+    dev = to_device(tr)
+    for correction in CORRECTIONS:
+        log_case(f"kernel agreement {correction}")
+        kw = dict(rho_bar=2.0, c_bar=1.0, lam=0.9, correction=correction, q_estimate="baseline",
+                  with_vs=True, with_pg_advantages=True)
+        a = vt.vtrace_loss_grad(**dev, **kw)
+        monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
+        b = vt.vtrace_loss_grad(**dev, **kw)
+        monkeypatch.delenv("VTRACE_KERNEL")
+        torch.cuda.synchronize()
+        for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+            assert_close(f"{correction} {name}", np_out(getattr(a, name)), np_out(getattr(b, name)),
+                         rtol=2e-5, atol=2e-6)
