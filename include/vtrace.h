@@ -101,10 +101,32 @@ typedef enum {
   VTRACE_Q_BASELINE = 1 /* q_s = r_s + gamma_s V(x_{s+1}) (App. E.3) */
 } vtrace_q_estimate;
 
+/*
+ * What the behaviour-policy argument holds.  The paper's actors send the
+ * behaviour policy's probabilities of the actions they took (Sec. 3); with
+ * LOG_PROBS the caller passes log mu(a_t|x_t) directly and the kernel reads
+ * 4 bytes per step instead of a whole logit row.
+ */
+typedef enum {
+  VTRACE_BEHAVIOUR_LOGITS = 0,   /* [T,B,A] logits of mu, in logits_dtype, 16-byte aligned */
+  VTRACE_BEHAVIOUR_LOG_PROBS = 1 /* [T,B] float32 log mu(a_t|x_t), 4-byte aligned */
+} vtrace_behaviour_input;
+
+/* Reward preprocessing applied inside the kernel (App. D). */
+typedef enum {
+  VTRACE_REWARD_RAW = 0,       /* rewards used as given */
+  VTRACE_REWARD_CLIP = 1,      /* clipped to [-1, 1] (single tasks) */
+  VTRACE_REWARD_ASYMMETRIC = 2 /* 0.3 min(tanh r, 0) + 5 max(tanh r, 0) (DMLab-30) */
+} vtrace_reward_transform;
+
 typedef struct {
-  int32_t correction; /* a vtrace_correction */
-  int32_t q_estimate; /* a vtrace_q_estimate */
-  float epsilon;      /* VTRACE_CORRECTION_EPSILON only: finite and > 0 (the paper uses 1e-6) */
+  int32_t correction;       /* a vtrace_correction */
+  int32_t q_estimate;       /* a vtrace_q_estimate */
+  float epsilon;            /* VTRACE_CORRECTION_EPSILON only: finite and > 0 (paper: 1e-6) */
+  int32_t behaviour_input;  /* a vtrace_behaviour_input */
+  int32_t reward_transform; /* a vtrace_reward_transform */
+  int32_t grad_dtype;       /* element type of d_logits: VTRACE_F32 or VTRACE_BF16 (rounded to
+                               nearest even); vtrace_loss_grad_ex only */
 } vtrace_variant;
 
 /* Version of this interface; bumped on any incompatible change. */
@@ -185,11 +207,12 @@ vtrace_status vtrace_loss_grad(
     void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
 
 /*
- * vtrace_targets / vtrace_loss_grad with a correction variant.  `variant` is a
- * HOST pointer read during the call (NULL = V-trace, the default); an unknown
- * correction or Q estimate, or a bad epsilon, gives VTRACE_ERR_PARAM.  NONE and
- * EPSILON do not use the importance ratio: behaviour_logits must still be a
- * valid [T,B,A] array, but its values do not change the outputs.
+ * vtrace_targets / vtrace_loss_grad with a variant.  `variant` is a HOST
+ * pointer read during the call (NULL = V-trace with the defaults above); an
+ * unknown enumerator or a bad epsilon gives VTRACE_ERR_PARAM.  NONE and EPSILON
+ * do not use the importance ratio: behaviour_logits must still be a valid
+ * array of the declared kind, but its values do not change the outputs.
+ * In vtrace_loss_grad_ex, d_logits has the element type variant->grad_dtype.
  */
 vtrace_status vtrace_targets_ex(
     int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
@@ -205,7 +228,7 @@ vtrace_status vtrace_loss_grad_ex(
     const float* rewards, const float* discounts, const float* values,
     const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
     float baseline_cost, float entropy_cost, const vtrace_variant* variant,
-    float* losses, float* d_logits, float* d_values,
+    float* losses, void* d_logits, float* d_values,
     float* vs, float* pg_advantages, float* lane_losses,
     void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
 

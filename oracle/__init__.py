@@ -22,4 +22,5 @@ from .definitions import (  # noqa: F401
     vtrace,
     loss_and_grads,
     total_loss_frozen_targets,
+    transform_rewards,
 )

@@ -66,19 +66,42 @@ def gather_action_logits(target_logits, behaviour_logits, actions):
     return np.stack([z, y], axis=-1)
 
 
-def truncated_is_weights(target_logits, behaviour_logits, actions, rho_bar, c_bar, lam):
+def transform_rewards(rewards, kind=None):
+    """Reward preprocessing of App. D: None leaves rewards as given; "clip" clips
+    them to [-1, 1] (single tasks); "asymmetric" is the optimistic asymmetric
+    clipping 0.3 min(tanh r, 0) + 5 max(tanh r, 0) (DMLab-30)."""
+    r = _f64(rewards)
+    if kind is None:
+        return r
+    if kind == "clip":
+        return np.clip(r, -1.0, 1.0)
+    if kind == "asymmetric":
+        t = np.tanh(r)
+        return 0.3 * np.minimum(t, 0.0) + 5.0 * np.maximum(t, 0.0)
+    raise ValueError(kind)
+
+
+def truncated_is_weights(target_logits, behaviour_logits, actions, rho_bar, c_bar, lam,
+                         behaviour="logits"):
     """Truncated importance weights of Sec. 4.1, with lambda as in Remark 2.
 
     rho_t = min(rho_bar, pi(a_t|x_t) / mu(a_t|x_t))
     c_t   = lambda * min(c_bar, pi(a_t|x_t) / mu(a_t|x_t))
-    Returns (log pi(a_t|x_t), log mu(a_t|x_t), rho, c).
+    ``behaviour_logits`` holds mu's logits [T, B, A], or, with
+    behaviour="log_probs", log mu(a_t|x_t) itself [T, B] (what the actors send,
+    Sec. 3).  Returns (log pi(a_t|x_t), log mu(a_t|x_t), rho, c).
     """
     a = np.asarray(actions, dtype=np.int64)
     A = np.shape(target_logits)[-1]
     if a.size and (a.min() < 0 or a.max() >= A):
         raise ValueError("action index out of range")
     log_pi_a = np.take_along_axis(log_softmax(target_logits), a[..., None], axis=-1)[..., 0]
-    log_mu_a = np.take_along_axis(log_softmax(behaviour_logits), a[..., None], axis=-1)[..., 0]
+    if behaviour == "logits":
+        log_mu_a = np.take_along_axis(log_softmax(behaviour_logits), a[..., None], axis=-1)[..., 0]
+    elif behaviour == "log_probs":
+        log_mu_a = _f64(behaviour_logits)
+    else:
+        raise ValueError(behaviour)
     ratio = np.exp(log_pi_a - log_mu_a)
     rho = np.minimum(np.float64(rho_bar), ratio)
     c = np.float64(lam) * np.minimum(np.float64(c_bar), ratio)
@@ -156,15 +179,19 @@ class VtraceOut(NamedTuple):
 
 def vtrace(target_logits, behaviour_logits, actions, rewards, discounts, values,
            bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, direct_sum=False,
-           correction="vtrace", q_estimate="vtrace") -> VtraceOut:
+           correction="vtrace", q_estimate="vtrace", behaviour="logits",
+           reward_transform=None) -> VtraceOut:
     """V-trace targets v_s and policy-gradient advantages for a [T, B] batch.
 
     ``rho`` and ``c`` in the result are always the truncated weights; which of
-    them enter the value target and the advantage depends on ``correction``."""
+    them enter the value target and the advantage depends on ``correction``.
+    ``behaviour`` says what ``behaviour_logits`` holds (see truncated_is_weights);
+    ``reward_transform`` preprocesses the rewards (see transform_rewards)."""
     if correction not in CORRECTIONS:
         raise ValueError(correction)
+    rewards = transform_rewards(rewards, reward_transform)
     log_pi_a, log_mu_a, rho, c = truncated_is_weights(
-        target_logits, behaviour_logits, actions, rho_bar, c_bar, lam)
+        target_logits, behaviour_logits, actions, rho_bar, c_bar, lam, behaviour)
     if correction == "vtrace":
         rho_value, c_value, rho_pg = rho, c, rho
     else:
@@ -217,12 +244,13 @@ def total_loss_frozen_targets(target_logits, values, actions, pg_adv, vs,
 def loss_and_grads(target_logits, behaviour_logits, actions, rewards, discounts, values,
                    bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0,
                    baseline_cost=0.5, entropy_cost=0.01, *, correction="vtrace",
-                   q_estimate="vtrace", epsilon=1e-6) -> LossGradOut:
+                   q_estimate="vtrace", epsilon=1e-6, behaviour="logits",
+                   reward_transform=None) -> LossGradOut:
     """The three losses of the V-trace actor-critic update (Sec. 4.2) and their
     gradients with respect to the target logits and the values."""
     vt = vtrace(target_logits, behaviour_logits, actions, rewards, discounts, values,
                 bootstrap_value, rho_bar, c_bar, lam, correction=correction,
-                q_estimate=q_estimate)
+                q_estimate=q_estimate, behaviour=behaviour, reward_transform=reward_transform)
     c_v = np.float64(baseline_cost)
     c_e = np.float64(entropy_cost)
     log_pi = log_softmax(target_logits)

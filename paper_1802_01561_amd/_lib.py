@@ -26,12 +26,16 @@ STATUS_NAMES = {
 
 CORRECTIONS = {"vtrace": 0, "none": 1, "epsilon": 2, "one_step_is": 3}
 Q_ESTIMATES = {"vtrace": 0, "baseline": 1}
+BEHAVIOUR_INPUTS = {"logits": 0, "log_probs": 1}
+REWARD_TRANSFORMS = {None: 0, "clip": 1, "asymmetric": 2}
 
 
 class Variant(ctypes.Structure):
-    """vtrace_variant: correction variant, Q estimate and epsilon."""
+    """vtrace_variant: correction, Q estimate, epsilon, behaviour input kind,
+    reward transform and gradient dtype."""
     _fields_ = [("correction", ctypes.c_int32), ("q_estimate", ctypes.c_int32),
-                ("epsilon", ctypes.c_float)]
+                ("epsilon", ctypes.c_float), ("behaviour_input", ctypes.c_int32),
+                ("reward_transform", ctypes.c_int32), ("grad_dtype", ctypes.c_int32)]
 
 
 # Every symbol include/vtrace.h declares, with (restype, argtypes).

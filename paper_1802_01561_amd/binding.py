@@ -12,7 +12,8 @@ from typing import NamedTuple, Optional
 
 import torch
 
-from ._lib import CORRECTIONS, Q_ESTIMATES, VTRACE_BF16, VTRACE_F32, Variant, check, lib
+from ._lib import (BEHAVIOUR_INPUTS, CORRECTIONS, Q_ESTIMATES, REWARD_TRANSFORMS, VTRACE_BF16,
+                   VTRACE_F32, Variant, check, lib)
 
 __all__ = [
     "LossGrad",
@@ -57,7 +58,8 @@ def _require(t: torch.Tensor, name: str, shape, dtype, device):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values, bootstrap_value):
+def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values, bootstrap_value,
+            behaviour="logits"):
     if target_logits.dim() != 3:
         raise ValueError("target_logits must be [T, B, A]")
     T, B, A = target_logits.shape
@@ -66,7 +68,10 @@ def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values
         raise ValueError("inputs must be on a GPU device")
     code = _dtype_code(target_logits)
     _require(target_logits, "target_logits", (T, B, A), None, dev)
-    _require(behaviour_logits, "behaviour_logits", (T, B, A), target_logits.dtype, dev)
+    if behaviour == "log_probs":
+        _require(behaviour_logits, "behaviour log-probabilities", (T, B), torch.float32, dev)
+    else:
+        _require(behaviour_logits, "behaviour_logits", (T, B, A), target_logits.dtype, dev)
     _require(actions, "actions", (T, B), torch.int32, dev)
     for name, t in (("rewards", rewards), ("discounts", discounts), ("values", values)):
         _require(t, name, (T, B), torch.float32, dev)
@@ -74,12 +79,15 @@ def _inputs(target_logits, behaviour_logits, actions, rewards, discounts, values
     return T, B, A, code, dev
 
 
-def _variant(correction, q_estimate, epsilon):
-    """A vtrace_variant for the _ex entry points (Sec. 5.2.3, App. E.3)."""
+def _variant(correction="vtrace", q_estimate="vtrace", epsilon=1e-6, behaviour="logits",
+             reward_transform=None, grad_dtype=torch.float32):
+    """A vtrace_variant for the _ex entry points (Sec. 5.2.3, App. D, App. E.3)."""
     try:
-        return Variant(CORRECTIONS[correction], Q_ESTIMATES[q_estimate], float(epsilon))
+        gd = {torch.float32: VTRACE_F32, torch.bfloat16: VTRACE_BF16}[grad_dtype]
+        return Variant(CORRECTIONS[correction], Q_ESTIMATES[q_estimate], float(epsilon),
+                       BEHAVIOUR_INPUTS[behaviour], REWARD_TRANSFORMS[reward_transform], gd)
     except KeyError as e:
-        raise ValueError(f"unknown correction or q_estimate: {e}") from None
+        raise ValueError(f"unknown variant setting: {e}") from None
 
 
 def vtrace_abi_version() -> int:
@@ -121,14 +129,17 @@ class LossGrad(NamedTuple):
 def vtrace_targets(target_logits, behaviour_logits, actions, rewards, discounts, values,
                    bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, *, vs=None,
                    pg_advantages=None, workspace: Optional[Workspace] = None, stream=None,
-                   correction="vtrace", q_estimate="vtrace", epsilon=1e-6):
+                   correction="vtrace", q_estimate="vtrace", epsilon=1e-6, behaviour="logits",
+                   reward_transform=None):
     """V-trace targets v_s and advantages; returns (vs, pg_advantages).
 
     ``correction`` ("vtrace", "none", "epsilon", "one_step_is") and
-    ``q_estimate`` ("vtrace", "baseline") select the paper's variants."""
-    variant = _variant(correction, q_estimate, epsilon)
+    ``q_estimate`` ("vtrace", "baseline") select the paper's variants;
+    behaviour="log_probs" takes ``behaviour_logits`` as [T, B] float32
+    log mu(a_t|x_t); ``reward_transform`` is None, "clip" or "asymmetric"."""
+    variant = _variant(correction, q_estimate, epsilon, behaviour, reward_transform)
     T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
-                                 values, bootstrap_value)
+                                 values, bootstrap_value, behaviour)
     if vs is None:
         vs = torch.empty((T, B), dtype=torch.float32, device=dev)
     if pg_advantages is None:
@@ -148,26 +159,28 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
                      entropy_cost=0.01, *, workspace: Optional[Workspace] = None,
                      with_vs=False, with_pg_advantages=False, with_lane_losses=False,
                      out: Optional[LossGrad] = None, stream=None, correction="vtrace",
-                     q_estimate="vtrace", epsilon=1e-6) -> LossGrad:
+                     q_estimate="vtrace", epsilon=1e-6, behaviour="logits",
+                     reward_transform=None, grad_dtype=torch.float32) -> LossGrad:
     """Fused V-trace targets, losses and gradients w.r.t. logits and values.
 
     ``out`` may hold preallocated output tensors (fields left None are skipped
-    when optional, allocated when required).  ``correction`` and ``q_estimate``
-    select the paper's variants, as in vtrace_targets."""
-    variant = _variant(correction, q_estimate, epsilon)
+    when optional, allocated when required).  The variant arguments are as in
+    vtrace_targets; ``grad_dtype`` (float32 or bfloat16) is d_logits' type."""
+    variant = _variant(correction, q_estimate, epsilon, behaviour, reward_transform, grad_dtype)
     T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
-                                 values, bootstrap_value)
+                                 values, bootstrap_value, behaviour)
     if workspace is None:
         workspace = Workspace(T, B, A, device=dev, stream=stream)
     if out is None:
         f32 = dict(dtype=torch.float32, device=dev)
         out = LossGrad(
-            torch.empty(4, **f32), torch.empty((T, B, A), **f32), torch.empty((T, B), **f32),
+            torch.empty(4, **f32), torch.empty((T, B, A), dtype=grad_dtype, device=dev),
+            torch.empty((T, B), **f32),
             torch.empty((T, B), **f32) if with_vs else None,
             torch.empty((T, B), **f32) if with_pg_advantages else None,
             torch.empty((B, 3), **f32) if with_lane_losses else None)
     _require(out.losses, "losses", (4,), torch.float32, dev)
-    _require(out.d_logits, "d_logits", (T, B, A), torch.float32, dev)
+    _require(out.d_logits, "d_logits", (T, B, A), grad_dtype, dev)
     _require(out.d_values, "d_values", (T, B), torch.float32, dev)
     if out.vs is not None:
         _require(out.vs, "vs", (T, B), torch.float32, dev)

@@ -62,7 +62,7 @@ vtrace_status check_common(int64_t T, int64_t B, int64_t A, vtrace_dtype dt, con
   if (!dtype_of(dt, lt)) return VTRACE_ERR_DTYPE;
   if (!truncation_ok(rho_bar) || !truncation_ok(c_bar)) return VTRACE_ERR_PARAM;
   if (std::isnan(lambda) || lambda < 0.0f || lambda > 1.0f) return VTRACE_ERR_PARAM;
-  if (!aligned(tl, 16) || !aligned(bl, 16)) return VTRACE_ERR_ALIGN;
+  if (!aligned(tl, 16) || !aligned(bl, 4)) return VTRACE_ERR_ALIGN;
   if (!aligned(act, 4) || !aligned(r, 4) || !aligned(d, 4) || !aligned(v, 4) || !aligned(boot, 4))
     return VTRACE_ERR_ALIGN;
   return VTRACE_OK;
@@ -101,15 +101,29 @@ vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
   a->correction = VTRACE_CORRECTION_VTRACE;
   a->q_estimate = VTRACE_Q_VTRACE;
   a->epsilon = 0.0f;
-  if (v == nullptr) return VTRACE_OK;
+  a->behaviour_log_probs = 0;
+  a->reward_transform = VTRACE_REWARD_RAW;
+  a->grad_bf16 = 0;
+  if (v == nullptr) return aligned(a->behaviour_logits, 16) ? VTRACE_OK : VTRACE_ERR_ALIGN;
   if (v->correction < VTRACE_CORRECTION_VTRACE || v->correction > VTRACE_CORRECTION_ONE_STEP_IS)
     return VTRACE_ERR_PARAM;
   if (v->q_estimate != VTRACE_Q_VTRACE && v->q_estimate != VTRACE_Q_BASELINE) return VTRACE_ERR_PARAM;
   if (v->correction == VTRACE_CORRECTION_EPSILON && !(std::isfinite(v->epsilon) && v->epsilon > 0.0f))
     return VTRACE_ERR_PARAM;
+  if (v->behaviour_input != VTRACE_BEHAVIOUR_LOGITS && v->behaviour_input != VTRACE_BEHAVIOUR_LOG_PROBS)
+    return VTRACE_ERR_PARAM;
+  if (v->reward_transform < VTRACE_REWARD_RAW || v->reward_transform > VTRACE_REWARD_ASYMMETRIC)
+    return VTRACE_ERR_PARAM;
+  if (v->grad_dtype != VTRACE_F32 && v->grad_dtype != VTRACE_BF16) return VTRACE_ERR_DTYPE;
+  // Logit rows are read with 16-byte vectors; log-probabilities are plain floats.
+  if (v->behaviour_input == VTRACE_BEHAVIOUR_LOGITS && !aligned(a->behaviour_logits, 16))
+    return VTRACE_ERR_ALIGN;
   a->correction = v->correction;
   a->q_estimate = v->q_estimate;
   a->epsilon = v->epsilon;
+  a->behaviour_log_probs = v->behaviour_input == VTRACE_BEHAVIOUR_LOG_PROBS;
+  a->reward_transform = v->reward_transform;
+  a->grad_bf16 = v->grad_dtype == VTRACE_BF16;
   return VTRACE_OK;
 }
 
@@ -227,7 +241,7 @@ vtrace_status vtrace_loss_grad_ex(int64_t T, int64_t B, int64_t A, vtrace_dtype 
                                   const float* discounts, const float* values,
                                   const float* bootstrap_value, float rho_bar, float c_bar,
                                   float lambda, float baseline_cost, float entropy_cost,
-                                  const vtrace_variant* variant, float* losses, float* d_logits,
+                                  const vtrace_variant* variant, float* losses, void* d_logits,
                                   float* d_values, float* vs, float* pg_advantages,
                                   float* lane_losses, void* workspace, size_t workspace_bytes,
                                   vtrace_stream_t stream) {

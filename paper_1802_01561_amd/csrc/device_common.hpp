@@ -59,6 +59,29 @@ __device__ __forceinline__ StepWeights variant_weights(int correction, double rh
   return w;
 }
 
+// Reward preprocessing of App. D (values of StepArgs::reward_transform).  NaN
+// stays NaN.
+constexpr int kRewardClip = 1, kRewardAsymmetric = 2;
+__device__ __forceinline__ float transform_reward(float r, int kind) {
+  if (kind == kRewardClip) return r < -1.0f ? -1.0f : (r > 1.0f ? 1.0f : r);
+  if (kind == kRewardAsymmetric) {
+    const float t = tanhf(r);
+    return t < 0.0f ? 0.3f * t : 5.0f * t;  // 0.3 min(t, 0) + 5 max(t, 0)
+  }
+  return r;
+}
+
+// Two floats to two bfloat16 (round to nearest even), packed low-first.
+typedef float v2f_t __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
+  const v2f_t f = {lo, hi};
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(f, v2bf_t));
+}
+__device__ __forceinline__ uint16_t to_bf16(float x) {
+  return static_cast<uint16_t>(pack_bf16x2(x, 0.0f) & 0xffffu);
+}
+
 // Butterfly sum over a wave.  Every lane ends with the same value, and the
 // order of additions is fixed, so the result is reproducible bit for bit.
 __device__ __forceinline__ double wave_sum(double v) {

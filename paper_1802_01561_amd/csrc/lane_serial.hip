@@ -21,6 +21,8 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
   const int64_t T = a.T, B = a.B, A = a.A;
   const In* __restrict__ zlog = static_cast<const In*>(a.target_logits);
   const In* __restrict__ ylog = static_cast<const In*>(a.behaviour_logits);
+  const float* __restrict__ lmu_g = static_cast<const float*>(a.behaviour_logits);
+  const bool beh_lp = a.behaviour_log_probs != 0;
   const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
   const float ce = a.entropy_cost;
 
@@ -40,12 +42,12 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
       float mz = -INFINITY, my = -INFINITY, za = 0.f, ya = 0.f;
       for (int64_t j = 0; j < A; ++j) {
         const float z = logit_to_float(zr[j]);
-        const float y = logit_to_float(yr[j]);
         mz = fmaxf(mz, z);
-        my = fmaxf(my, y);
-        if (j == act) {
-          za = z;
-          ya = y;
+        if (j == act) za = z;
+        if (!beh_lp) {
+          const float y = logit_to_float(yr[j]);
+          my = fmaxf(my, y);
+          if (j == act) ya = y;
         }
       }
       // Exponent sums; also sum_j e_j (z_j - m_z), which gives the entropy as
@@ -58,15 +60,21 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
         sz += e;
         ed += e * dz;
         if (j == act) ea = e;
-        sy += expf(logit_to_float(yr[j]) - my);
+        if (!beh_lp) sy += expf(logit_to_float(yr[j]) - my);
       }
 
-      const double ratio = valid ? importance_ratio(za, mz, ya, my, sz, sy) : NAN;
+      // With behaviour log-probabilities the ratio is exp(log pi(a) - log mu(a)).
+      const double ratio =
+          !valid ? NAN
+          : beh_lp ? exp(static_cast<double>(za) - static_cast<double>(mz) - log(sz) -
+                         static_cast<double>(lmu_g[idx]))
+                   : importance_ratio(za, mz, ya, my, sz, sy);
       if (!valid) raise_error_flag(a.error_flag);
       const StepWeights w = variant_weights(a.correction, clip_above(ratio, rho_bar),
                                             lam * clip_above(ratio, c_bar), lam, valid);
 
-      const double r = a.rewards[idx], g = a.discounts[idx], V = a.values[idx];
+      const double r = transform_reward(a.rewards[idx], a.reward_transform);
+      const double g = a.discounts[idx], V = a.values[idx];
       const double delta = w.rho_v * (r + g * V_next - V);
       const double A_t = delta + g * w.c_v * A_next;  // v_t - V(x_t)
       const double v_t = V + A_t;
@@ -89,12 +97,15 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
         const bool eps_mode = a.correction == kCorrEpsilon;
         const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
         const float adv32 = valid ? static_cast<float>(adv) * pg_w : NAN;
-        float* dl = a.d_logits + idx * A;
         for (int64_t j = 0; j < A; ++j) {
           const float dz = logit_to_float(zr[j]) - mz;
           const float p = expf(dz) * inv;
           const float pg_term = (j == act) ? -one_minus_pa : p;
-          dl[j] = adv32 * pg_term + ce * p * ((dz - log_s) + H);
+          const float d = adv32 * pg_term + ce * p * ((dz - log_s) + H);
+          if (a.grad_bf16)
+            static_cast<uint16_t*>(a.d_logits)[idx * A + j] = to_bf16(d);
+          else
+            static_cast<float*>(a.d_logits)[idx * A + j] = d;
         }
         const double log_pa = !valid ? NAN
                               : eps_mode ? static_cast<double>(logf(pa + a.epsilon))

@@ -24,9 +24,15 @@ struct StepArgs {
   // Q estimate (0: r + gamma v_{s+1}, 1: r + gamma V(x_{s+1})) and epsilon.
   int correction, q_estimate;
   float epsilon;
+  // 1: behaviour_logits holds [T,B] float32 log mu(a_t|x_t) instead of logits.
+  int behaviour_log_probs;
+  // Reward preprocessing: 0 none, 1 clip to [-1, 1], 2 optimistic asymmetric.
+  int reward_transform;
+  // 1: d_logits is written as bfloat16.
+  int grad_bf16;
   // outputs (any may be null except where a kernel variant requires them)
   float* losses;       // [4]
-  float* d_logits;     // [T,B,A]
+  void* d_logits;      // [T,B,A] float32 or bfloat16
   float* d_values;     // [T,B]
   float* vs;           // [T,B]
   float* pg_adv;       // [T,B]

@@ -125,6 +125,7 @@ struct Tile {
   static_assert((SEG * int(sizeof(In))) % 16 == 0, "logit rows must be whole 16-byte vectors");
   static_assert((SEG * 4) % 16 == 0, "gradient rows must be whole 16-byte vectors");
   static_assert(NT % kWave == 0 && NT <= 1024, "bad workgroup size");
+  static_assert(OUT_ROW16 % 2 == 0, "bfloat16 gradient rows must be whole 16-byte vectors");
 };
 
 // Per-thread state carried along the chunk walk.
@@ -149,18 +150,24 @@ struct RowStats {
 // amplified; the exponent sums are then formed from float64 exponentials of
 // exact float64 differences.  Otherwise every weight is at most 1, nothing is
 // amplified, and float32 exponentials are accurate enough.
+//
+// With behaviour log-probabilities (beh_lp) there is no behaviour row: the
+// ratio is exp(log pi(a|x) - lmu), lmu = log mu(a|x) as given.
 template <int A_, bool kPrecise, typename In>
 __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
-                                              float (&e)[A_]) {
+                                              bool beh_lp, float lmu, float (&e)[A_]) {
   RowStats st;
   const float za = logit_to_float(zr[act_c]);
-  const float ya = logit_to_float(yr[act_c]);
   float mz = logit_to_float(zr[0]);
 #pragma unroll
   for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
-  float my = logit_to_float(yr[0]);
+  float ya = 0.f, my = 0.f;
+  if (!beh_lp) {
+    ya = logit_to_float(yr[act_c]);
+    my = logit_to_float(yr[0]);
 #pragma unroll
-  for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
+    for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
+  }
   st.mz = mz;
   float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
   if constexpr (kPrecise) {
@@ -173,14 +180,18 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
       e[j] = static_cast<float>(x);
       ed = fmaf(e[j], static_cast<float>(d), ed);
     }
-#pragma unroll
-    for (int j = 0; j < A_; ++j)
-      sy += exp_nonpos_f64(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
     const double inv = 1.0 / sz;
     const double dza = static_cast<double>(za) - static_cast<double>(mz);
-    const double dya = static_cast<double>(ya) - static_cast<double>(my);
     const double ea = exp_nonpos_f64(dza);
-    st.ratio = act_ok ? exp(dza - dya) * (sy * inv) : NAN;
+    if (beh_lp) {
+      st.ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
+    } else {
+#pragma unroll
+      for (int j = 0; j < A_; ++j)
+        sy += exp_nonpos_f64(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
+      const double dya = static_cast<double>(ya) - static_cast<double>(my);
+      st.ratio = act_ok ? exp(dza - dya) * (sy * inv) : NAN;
+    }
     st.inv_s = static_cast<float>(inv);
     st.log_s = static_cast<float>(log(sz));
     st.one_minus_pa = static_cast<float>((sz - ea) * inv);
@@ -194,13 +205,18 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
       sz += e[j];
       ed = fmaf(e[j], d, ed);
     }
-#pragma unroll
-    for (int j = 0; j < A_; ++j) sy += exp_fast(logit_to_float(yr[j]) - my);
     const float inv = __builtin_amdgcn_rcpf(sz);
     const float ea = exp_fast(za - mz);
-    st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
+    const float log_s = __logf(sz);
+    if (beh_lp) {
+      st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - log_s - lmu)) : NAN;
+    } else {
+#pragma unroll
+      for (int j = 0; j < A_; ++j) sy += exp_fast(logit_to_float(yr[j]) - my);
+      st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
+    }
     st.inv_s = inv;
-    st.log_s = __logf(sz);
+    st.log_s = log_s;
     st.one_minus_pa = (sz - ea) * inv;
     st.e_a = ea;
   }
@@ -225,18 +241,22 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
   const int nchunks = static_cast<int>((T + kL - 1) / kL);
 
-  // Byte strides of one time row.
+  // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
-  const int64_t out_row = B * A_ * 4;
+  const bool beh_lp = a.behaviour_log_probs != 0;
+  const bool grad_bf16 = a.grad_bf16 != 0;
+  const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
+  const int64_t out_row = B * A_ * gsz;
   const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
   const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
-  char* const dg = reinterpret_cast<char*>(a.d_logits) + b0 * A_ * 4;
+  const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
+  char* const dg = static_cast<char*>(a.d_logits) + b0 * A_ * gsz;
 
   // Register prefetch (vector path): NV 16-byte vectors covering both tensors,
   // plus this thread's action, reward, discount and value.
   v4u pre[S::NV];
   int32_t p_act = 0;
-  float p_r = 0.f, p_g = 0.f, p_V = 0.f;
+  float p_r = 0.f, p_g = 0.f, p_V = 0.f, p_lmu = 0.f;
 
   auto prefetch = [&](int k) {
     const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
@@ -244,8 +264,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     static_for<S::NV>([&](auto I) {
       constexpr int i = decltype(I)::value;
       const int f = tid + i * NT;
-      if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) {
-        const bool is_y = f >= S::IN_TILE16;
+      const bool is_y = f >= S::IN_TILE16;
+      if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && beh_lp)) {
         const int g = is_y ? f - S::IN_TILE16 : f;
         int r = g / S::IN_ROW16;
         const int c = g % S::IN_ROW16;
@@ -263,6 +283,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       p_r = a.rewards[idx];
       p_g = a.discounts[idx];
       p_V = a.values[idx];
+      if (beh_lp) p_lmu = lmu_g[idx];
     }
   };
 
@@ -278,13 +299,13 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
 
     __syncthreads();  // the previous chunk is done with LDS
     int32_t act;
-    float r32, g32, V32;
+    float r32, g32, V32, lmu = 0.f;
     if constexpr (kVec) {
       static_for<S::NV>([&](auto I) {
         constexpr int i = decltype(I)::value;
         const int f = tid + i * NT;
-        if (i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) {
-          const bool is_y = f >= S::IN_TILE16;
+        const bool is_y = f >= S::IN_TILE16;
+        if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && beh_lp)) {
           const int g = is_y ? f - S::IN_TILE16 : f;
           const int r = g / S::IN_ROW16, c = g % S::IN_ROW16;
           lds[(is_y ? S::IN_LDS16 : 0) + r * S::IN_PITCH16 + c] = pre[i];
@@ -294,6 +315,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       r32 = p_r;
       g32 = p_g;
       V32 = p_V;
+      lmu = p_lmu;
       __syncthreads();
       if (k + 1 < nchunks) prefetch(k + 1);
     } else {
@@ -305,7 +327,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         if (te >= 0 && c < nb * A_) {
           const int64_t off = (te * B + b0) * A_ + c;
           lz[rr * S::IN_PITCH + c] = static_cast<const In*>(a.target_logits)[off];
-          ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
+          if (!beh_lp) ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
         }
       }
       act = 0;
@@ -315,9 +337,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         r32 = a.rewards[idx];
         g32 = a.discounts[idx];
         V32 = a.values[idx];
+        if (beh_lp) lmu = lmu_g[idx];
       }
       __syncthreads();
     }
+    r32 = transform_reward(r32, a.reward_transform);
     if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
 
     // This thread's rows.
@@ -327,7 +351,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
     float e[A_];
-    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, e);
+    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, lmu, e);
     const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
@@ -403,24 +427,49 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       __syncthreads();
       if constexpr (kVec) {
         const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
-        static_for<S::NO>([&](auto I) {
-          constexpr int i = decltype(I)::value;
-          const int f = tid + i * NT;
-          if (i * NT + NT <= S::OUT_TILE16 || f < S::OUT_TILE16) {
-            const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
-            if (rr >= neg)
-              __builtin_nontemporal_store(
-                  lds[rr * S::OUT_PITCH16 + cc],
-                  reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+        if (!grad_bf16) {
+          static_for<S::NO>([&](auto I) {
+            constexpr int i = decltype(I)::value;
+            const int f = tid + i * NT;
+            if (i * NT + NT <= S::OUT_TILE16 || f < S::OUT_TILE16) {
+              const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
+              if (rr >= neg)
+                __builtin_nontemporal_store(
+                    lds[rr * S::OUT_PITCH16 + cc],
+                    reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+            }
+          });
+        } else {
+          // bfloat16 rows: each 16-byte store packs two 16-byte LDS vectors.
+          constexpr int kRow16 = S::OUT_ROW16 / 2, kTile16 = S::OUT_TILE16 / 2;
+          for (int f = tid; f < kTile16; f += NT) {
+            const int rr = f / kRow16, cc = f % kRow16;
+            if (rr >= neg) {
+              const v4u lo = lds[rr * S::OUT_PITCH16 + 2 * cc];
+              const v4u hi = lds[rr * S::OUT_PITCH16 + 2 * cc + 1];
+              v4u pk;
+              pk.x = pack_bf16x2(__uint_as_float(lo.x), __uint_as_float(lo.y));
+              pk.y = pack_bf16x2(__uint_as_float(lo.z), __uint_as_float(lo.w));
+              pk.z = pack_bf16x2(__uint_as_float(hi.x), __uint_as_float(hi.y));
+              pk.w = pack_bf16x2(__uint_as_float(hi.z), __uint_as_float(hi.w));
+              __builtin_nontemporal_store(pk,
+                                          reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+            }
           }
-        });
+        }
       } else {
         const float* lf = reinterpret_cast<const float*>(lds);
         for (int e2 = tid; e2 < kL * S::SEG; e2 += NT) {
           const int rr = e2 / S::SEG, cc = e2 % S::SEG;
           const int64_t te = t0 + rr;
-          if (te >= 0 && cc < nb * A_)
-            a.d_logits[(te * B + b0) * A_ + cc] = lf[rr * S::OUT_PITCH + cc];
+          if (te >= 0 && cc < nb * A_) {
+            const float x = lf[rr * S::OUT_PITCH + cc];
+            const int64_t o = (te * B + b0) * A_ + cc;
+            if (grad_bf16)
+              static_cast<uint16_t*>(a.d_logits)[o] = to_bf16(x);
+            else
+              static_cast<float*>(a.d_logits)[o] = x;
+          }
         }
       }
     }
@@ -498,7 +547,7 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
   *nwg = blocks;
   // Vector path: full lane tiles whose time rows start on 16-byte boundaries.
   const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
-  const int64_t out_row = a.B * A_ * 4;
+  const int64_t out_row = a.B * A_ * (a.grad_bf16 ? 2 : 4);
   const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
   const int64_t vec_tiles = aligned ? a.B / LANES : 0;
   if (mode == Mode::LossGrad)

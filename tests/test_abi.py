@@ -148,9 +148,16 @@ def test_variant_validation(L):
                                    variant, P, P, None, 0, None)
 
     for bad in (V(4, 0, 1e-6), V(-1, 0, 1e-6), V(0, 2, 1e-6), V(0, -1, 1e-6), V(2, 0, 0.0),
-                V(2, 0, -1e-6), V(2, 0, math.nan), V(2, 0, math.inf)):
+                V(2, 0, -1e-6), V(2, 0, math.nan), V(2, 0, math.inf), V(0, 0, 0.0, 2, 0, 0),
+                V(0, 0, 0.0, -1, 0, 0), V(0, 0, 0.0, 0, 3, 0), V(0, 0, 0.0, 0, -1, 0)):
         assert loss_ex(ctypes.byref(bad)) == PARAM
         assert targets_ex(ctypes.byref(bad)) == PARAM
+    assert loss_ex(ctypes.byref(V(0, 0, 0.0, 0, 0, 2))) == DTYPE
+    # behaviour logits need 16-byte alignment, behaviour log-probabilities 4
+    assert loss_ex(None, bl=P + 4, ws=None) == WS
+    assert loss_ex(None, bl=P + 4) == ALIGN
+    assert loss_ex(ctypes.byref(V(0, 0, 0.0, 1, 0, 0)), bl=P + 4, T=0) == SHAPE
+    assert loss_ex(ctypes.byref(V(0, 0, 0.0, 1, 0, 0)), bl=P + 2) == ALIGN
     # a valid variant with another invalid argument is still rejected before launch
     for good in (None, ctypes.byref(V(0, 0, 0.0)), ctypes.byref(V(3, 1, 0.0)),
                  ctypes.byref(V(2, 0, 1e-6))):
@@ -161,10 +168,16 @@ def test_variant_validation(L):
 
 def test_python_variant_names():
     from paper_1802_01561_amd import binding
+    import torch
     assert binding._variant("one_step_is", "baseline", 1e-6).correction == 3
     assert binding._variant("epsilon", "vtrace", 1e-6).q_estimate == 0
-    with pytest.raises(ValueError):
-        binding._variant("retrace", "vtrace", 1e-6)
+    v = binding._variant(behaviour="log_probs", reward_transform="asymmetric",
+                         grad_dtype=torch.bfloat16)
+    assert (v.behaviour_input, v.reward_transform, v.grad_dtype) == (1, 2, 1)
+    for bad in (dict(correction="retrace"), dict(behaviour="probs"), dict(reward_transform="tanh"),
+                dict(grad_dtype=torch.float16)):
+        with pytest.raises(ValueError):
+            binding._variant(**bad)
 
 
 def test_gather_and_flag_reject(L):

@@ -98,3 +98,98 @@ def test_variant_kernels_agree(monkeypatch):
         for name in ("vs", "pg_advantages", "d_values", "d_logits"):
             assert_close(f"{correction} {name}", np_out(getattr(a, name)), np_out(getattr(b, name)),
                          rtol=2e-5, atol=2e-6)
+
+
+# --------------------------------------------------------------------------------------
+# Input/output variants: behaviour log-probabilities, reward preprocessing, bf16 grads
+# --------------------------------------------------------------------------------------
+
+# bfloat16 gradients: the float32 result (within 1e-5 + 1e-4|o| of the oracle) is
+# rounded to nearest-even bfloat16 (8 significant bits), adding at most 2^-8 of
+# its magnitude, so
+# |g - o| <= 1e-5 + 1e-4|o| + 2^-8 (1 + 1e-4)|o| + 2^-8 * 1e-5 < 1.1e-5 + 4.1e-3|o|.
+BF16_GRAD_ATOL, BF16_GRAD_RTOL = 1.1e-5, 4.1e-3
+
+
+def behaviour_log_probs(tr):
+    """log mu(a_t|x_t) as float32, from the behaviour logits (host, float64)."""
+    import scipy.special
+    lp = scipy.special.log_softmax(tr.behaviour_logits.astype(np.float64), axis=-1)
+    return np.take_along_axis(lp, tr.actions[..., None].astype(np.int64), -1)[..., 0].astype(np.float32)
+
+
+def check_io_variant(tr, p, *, log_probs=False, reward_transform=None, grad_bf16=False,
+                     correction="vtrace", lanes=None):
+    dev = to_device(tr)
+    otr_args = list(oracle_args(tr))
+    behaviour = "logits"
+    if log_probs:
+        lmu = behaviour_log_probs(tr)
+        dev["behaviour_logits"] = torch.from_numpy(lmu).cuda()
+        otr_args[1] = lmu
+        behaviour = "log_probs"
+    gd = torch.bfloat16 if grad_bf16 else torch.float32
+    out = vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                              baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
+                              with_vs=True, with_pg_advantages=True, with_lane_losses=True,
+                              correction=correction, behaviour=behaviour,
+                              reward_transform=reward_transform, grad_dtype=gd)
+    vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                               correction=correction, behaviour=behaviour,
+                               reward_transform=reward_transform)
+    torch.cuda.synchronize()
+    if lanes is not None:
+        idx = np.asarray(lanes)
+        otr_args = [x[:, idx] if i != 6 else x[idx] for i, x in enumerate(otr_args)]
+    o = oracle.loss_and_grads(*otr_args, p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
+                              p.entropy_cost, correction=correction, behaviour=behaviour,
+                              reward_transform=reward_transform)
+    pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
+    tag = f"lp={log_probs} r={reward_transform} bf16={grad_bf16} {correction}"
+    assert_close(f"{tag} vs", pick(np_out(out.vs)), o.vs)
+    assert_close(f"{tag} pg_advantages", pick(np_out(out.pg_advantages)), o.pg_advantages)
+    assert_close(f"{tag} d_values", pick(np_out(out.d_values)), o.d_values)
+    dl_kw = dict(rtol=BF16_GRAD_RTOL, atol=BF16_GRAD_ATOL) if grad_bf16 else {}
+    assert out.d_logits.dtype == gd
+    assert_close(f"{tag} d_logits", pick(np_out(out.d_logits)), o.d_logits, **dl_kw)
+    lane = np_out(out.lane_losses)
+    assert_close(f"{tag} lane_losses", lane if lanes is None else lane[lanes], o.lane_losses)
+    if lanes is None:
+        assert_close(f"{tag} losses", np_out(out.losses), o.losses)
+        assert_close(f"{tag} targets.vs", np_out(vs), o.vs)
+        assert_close(f"{tag} targets.pg_advantages", np_out(pg), o.pg_advantages)
+
+
+@pytest.mark.parametrize("log_probs", [False, True])
+@pytest.mark.parametrize("reward_transform", [None, "clip", "asymmetric"])
+@pytest.mark.parametrize("grad_bf16", [False, True])
+def test_io_variants_configs(log_probs, reward_transform, grad_bf16):
+    for cfg in (1, 2):
+        tr = make_config(cfg)
+        tr.rewards = (tr.rewards * 3.0 - 0.5).astype(np.float32)  # exercise the clipping
+        for p in (Params(1.0, 1.0, 1.0), Params(math.inf, math.inf, 1.0)):
+            log_case(f"config {cfg} io lp={log_probs} r={reward_transform} bf16={grad_bf16} {p.label()}")
+            check_io_variant(tr, p, log_probs=log_probs, reward_transform=reward_transform,
+                             grad_bf16=grad_bf16)
+
+
+@pytest.mark.parametrize("shape", [(37, 45, 18), (33, 70, 9), (12, 10, 7), (20, 64, 18)])
+@pytest.mark.parametrize("bf16_logits", [False, True])
+def test_io_variants_shapes(shape, bf16_logits):
+    T, B, A = shape
+    tr = make_random(T, B, A, 300 + T + A, noise_std=1.0, bf16=bf16_logits)
+    tr.rewards = (tr.rewards * 2.5).astype(np.float32)
+    for correction in ("vtrace", "one_step_is", "epsilon"):
+        log_case(f"io variants T={T} B={B} A={A} bf16-logits={bf16_logits} {correction}")
+        check_io_variant(tr, Params(1.0, 0.5, 0.95), log_probs=True, reward_transform="asymmetric",
+                         grad_bf16=True, correction=correction)
+        check_io_variant(tr, Params(2.0, 1.0, 1.0), log_probs=False, reward_transform="clip",
+                         grad_bf16=True, correction=correction)
+
+
+def test_io_variants_stress_subset():
+    from synth.trajectories import STRESS_SUBSET
+    tr = make_config(4)
+    for p in (Params(1.0, 1.0, 1.0), Params(math.inf, math.inf, 1.0)):
+        log_case(f"stress, behaviour log-probabilities + bf16 grads, {p.label()}")
+        check_io_variant(tr, p, log_probs=True, grad_bf16=True, lanes=STRESS_SUBSET)

@@ -231,3 +231,53 @@ def test_unmutated_oracle_passes_variant_pins():
 @pytest.mark.parametrize("name", sorted(VARIANT_MUTATIONS))
 def test_planted_variant_mistake_is_caught(name):
     assert not _variant_pins_pass(_mutant(VARIANT_MUTATIONS[name]))
+
+
+# --------------------------------------------------------------------------------------
+# Input/output variants: behaviour log-probabilities, reward preprocessing
+# --------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("correction", ["vtrace", "one_step_is", "epsilon"])
+def test_behaviour_log_probs_input(seed, correction):
+    """Passing log mu(a_t|x_t) (here from scipy's log-softmax) instead of mu's
+    logits gives the same result."""
+    tr = _batch(seed)
+    lmu = np.take_along_axis(scipy.special.log_softmax(tr.behaviour_logits.astype(np.float64), -1),
+                             tr.actions[..., None].astype(np.int64), -1)[..., 0]
+    a = oracle.loss_and_grads(*_args(tr), 2.0, 1.0, 0.9, correction=correction)
+    args = list(_args(tr))
+    args[1] = lmu
+    b = oracle.loss_and_grads(*args, 2.0, 1.0, 0.9, correction=correction, behaviour="log_probs")
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, rtol=1e-12, atol=1e-13)
+
+
+def test_reward_transforms():
+    r = np.array([-50.0, -1.5, -1.0, -0.3, 0.0, 0.4, math.atanh(0.5), 1.0, 2.0, 80.0])
+    clip = ov.transform_rewards(r, "clip")
+    assert clip.tolist() == [-1.0, -1.0, -1.0, -0.3, 0.0, 0.4, math.atanh(0.5), 1.0, 1.0, 1.0]
+    asym = ov.transform_rewards(r, "asymmetric")
+    # 0.3 min(tanh r, 0) + 5 max(tanh r, 0): 0 at 0, 2.5 where tanh r = 1/2, limits -0.3 and 5
+    assert asym[4] == 0.0
+    assert asym[6] == pytest.approx(2.5, rel=1e-15)
+    assert asym[0] == pytest.approx(-0.3, rel=1e-15) and asym[-1] == pytest.approx(5.0, rel=1e-15)
+    assert asym[3] == pytest.approx(0.3 * math.tanh(-0.3), rel=1e-15)
+    assert np.all(np.diff(asym) >= 0)
+    assert ov.transform_rewards(r, None).tolist() == r.tolist()
+    with pytest.raises(ValueError):
+        ov.transform_rewards(r, "tanh")
+
+
+@pytest.mark.parametrize("kind", ["clip", "asymmetric"])
+def test_reward_transform_is_applied_first(kind):
+    """The preprocessed batch equals the raw batch with transformed rewards."""
+    tr = _batch(3)
+    tr.rewards = (tr.rewards * 4).astype(np.float32)
+    a = oracle.loss_and_grads(*_args(tr), 1.0, 1.0, 1.0, reward_transform=kind)
+    args = list(_args(tr))
+    args[3] = np.clip(tr.rewards.astype(np.float64), -1, 1) if kind == "clip" else \
+        np.where(tr.rewards < 0, 0.3, 5.0) * np.tanh(tr.rewards.astype(np.float64))
+    b = oracle.loss_and_grads(*args, 1.0, 1.0, 1.0)
+    for x, y in zip(a, b):
+        np.testing.assert_allclose(x, y, rtol=1e-13, atol=1e-14)
