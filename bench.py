@@ -40,6 +40,12 @@ def parse_args():
     ap.add_argument("--params", type=int, default=0, help="parameter set of the workload")
     ap.add_argument("--bf16", action="store_true", help="bfloat16 logits")
     ap.add_argument("--kernel", choices=["auto", "lane_serial"], default="auto")
+    ap.add_argument("--correction", choices=["vtrace", "none", "epsilon", "one_step_is"],
+                    default="vtrace")
+    ap.add_argument("--log-probs", action="store_true",
+                    help="pass log mu(a_t|x_t) [T,B] instead of mu's logits")
+    ap.add_argument("--grad-bf16", action="store_true", help="bfloat16 d_logits")
+    ap.add_argument("--reward-transform", choices=["clip", "asymmetric"], default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
@@ -101,10 +107,13 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(T, B, A, logit_bytes):
-    """Bytes one call must move: both logit rows, action, reward, discount and
-    value in; d_logits (fp32) and d_values out; plus the bootstrap values."""
-    per_step = 2 * A * logit_bytes + 16 + 4 * A + 4
+def algorithmic_bytes(T, B, A, logit_bytes, log_probs=False, grad_bytes=4, uses_mu=True):
+    """Bytes one call must move: the target logit row, the behaviour logit row
+    (or one log-probability; nothing for variants that ignore mu), action,
+    reward, discount and value in; d_logits and d_values out; plus the
+    bootstrap values."""
+    behaviour = 0 if not uses_mu else (4 if log_probs else A * logit_bytes)
+    per_step = A * logit_bytes + behaviour + 16 + A * grad_bytes + 4
     return T * B * per_step + 4 * B, per_step
 
 
@@ -215,19 +224,28 @@ def main():
     p = PARAM_SETS[args.config][args.params]
     dev = to_device(tr, torch, np)
     T, B, A = tr.T, tr.B, tr.A
+    behaviour = "logits"
+    if args.log_probs:
+        # log mu(a_t|x_t), computed once on the device outside the timed region
+        lp = torch.log_softmax(dev["behaviour_logits"].float(), dim=-1)
+        dev["behaviour_logits"] = lp.gather(-1, dev["actions"].long()[..., None])[..., 0].contiguous()
+        del lp
+        behaviour = "log_probs"
+    grad_dtype = torch.bfloat16 if args.grad_bf16 else torch.float32
     print(f"[bench] {tr.name} T={T} B={B} A={A} {tr.dtype} {p.label()} "
           f"(generated+uploaded in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
 
     ws = vt.Workspace(T, B, A)
     f32 = dict(dtype=torch.float32, device="cuda")
-    out = vt.LossGrad(torch.empty(4, **f32), torch.empty((T, B, A), **f32),
+    out = vt.LossGrad(torch.empty(4, **f32), torch.empty((T, B, A), dtype=grad_dtype, device="cuda"),
                       torch.empty((T, B), **f32), None, None, None)
     stream = torch.cuda.current_stream()
 
     def step():
         vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
                             baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
-                            workspace=ws, out=out)
+                            workspace=ws, out=out, correction=args.correction, behaviour=behaviour,
+                            reward_transform=args.reward_transform, grad_dtype=grad_dtype)
 
     for _ in range(args.warmup):
         step()
@@ -249,7 +267,9 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / K
     steps_per_s = T * B / (ms_per_step * 1e-3)
     logit_bytes = 2 if args.bf16 else 4
-    alg_bytes, per_step = algorithmic_bytes(T, B, A, logit_bytes)
+    alg_bytes, per_step = algorithmic_bytes(T, B, A, logit_bytes, args.log_probs,
+                                            2 if args.grad_bf16 else 4,
+                                            args.correction in ("vtrace", "one_step_is"))
     avg_kernel_ms = float(kernel_ms.mean())
     achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
     losses = out.losses.cpu().tolist()
@@ -258,7 +278,9 @@ def main():
           f"algorithmic; losses {losses}", file=sys.stderr, flush=True)
 
     is_counted_workload = (args.config == 4 and args.params == 0 and not args.bf16
-                           and args.kernel == "auto")
+                           and args.kernel == "auto" and args.correction == "vtrace"
+                           and not args.log_probs and not args.grad_bf16
+                           and args.reward_transform is None)
     traffic, traffic_bytes = stored_traffic(avg_kernel_ms) if is_counted_workload else (None, None)
     result = {
         "metric": METRIC,
@@ -275,7 +297,11 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{tr.name}: T={T} B={B} A={A} {tr.dtype} logits, "
-                        f"rho_bar={p.rho_bar} c_bar={p.c_bar} lambda={p.lam}",
+                        f"rho_bar={p.rho_bar} c_bar={p.c_bar} lambda={p.lam}"
+                        + (f", correction={args.correction}" if args.correction != "vtrace" else "")
+                        + (", behaviour log-probs" if args.log_probs else "")
+                        + (", bf16 d_logits" if args.grad_bf16 else "")
+                        + (f", rewards {args.reward_transform}" if args.reward_transform else ""),
             "T": T, "B": B, "A": A, "logits": tr.dtype,
             "rho_bar": p.rho_bar if math.isfinite(p.rho_bar) else "inf",
             "c_bar": p.c_bar if math.isfinite(p.c_bar) else "inf",

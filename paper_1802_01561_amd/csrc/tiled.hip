@@ -152,17 +152,19 @@ struct RowStats {
 // amplified, and float32 exponentials are accurate enough.
 //
 // With behaviour log-probabilities (beh_lp) there is no behaviour row: the
-// ratio is exp(log pi(a|x) - lmu), lmu = log mu(a|x) as given.
+// ratio is exp(log pi(a|x) - lmu), lmu = log mu(a|x) as given.  Variants that
+// do not use the ratio (no_ratio) skip the behaviour row too; their ratio is 1.
 template <int A_, bool kPrecise, typename In>
 __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
-                                              bool beh_lp, float lmu, float (&e)[A_]) {
+                                              bool beh_lp, bool no_ratio, float lmu,
+                                              float (&e)[A_]) {
   RowStats st;
   const float za = logit_to_float(zr[act_c]);
   float mz = logit_to_float(zr[0]);
 #pragma unroll
   for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
   float ya = 0.f, my = 0.f;
-  if (!beh_lp) {
+  if (!beh_lp && !no_ratio) {
     ya = logit_to_float(yr[act_c]);
     my = logit_to_float(yr[0]);
 #pragma unroll
@@ -183,7 +185,9 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
     const double inv = 1.0 / sz;
     const double dza = static_cast<double>(za) - static_cast<double>(mz);
     const double ea = exp_nonpos_f64(dza);
-    if (beh_lp) {
+    if (no_ratio) {
+      st.ratio = act_ok ? 1.0 : NAN;
+    } else if (beh_lp) {
       st.ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
     } else {
 #pragma unroll
@@ -208,7 +212,9 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
     const float inv = __builtin_amdgcn_rcpf(sz);
     const float ea = exp_fast(za - mz);
     const float log_s = __logf(sz);
-    if (beh_lp) {
+    if (no_ratio) {
+      st.ratio = act_ok ? 1.0 : NAN;
+    } else if (beh_lp) {
       st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - log_s - lmu)) : NAN;
     } else {
 #pragma unroll
@@ -244,6 +250,9 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
   const bool beh_lp = a.behaviour_log_probs != 0;
+  // No-correction and epsilon-correction never look at the behaviour policy.
+  const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
+  const bool skip_y = beh_lp || no_ratio;
   const bool grad_bf16 = a.grad_bf16 != 0;
   const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
   const int64_t out_row = B * A_ * gsz;
@@ -265,7 +274,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       constexpr int i = decltype(I)::value;
       const int f = tid + i * NT;
       const bool is_y = f >= S::IN_TILE16;
-      if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && beh_lp)) {
+      if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
         const int g = is_y ? f - S::IN_TILE16 : f;
         int r = g / S::IN_ROW16;
         const int c = g % S::IN_ROW16;
@@ -283,7 +292,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       p_r = a.rewards[idx];
       p_g = a.discounts[idx];
       p_V = a.values[idx];
-      if (beh_lp) p_lmu = lmu_g[idx];
+      if (beh_lp && !no_ratio) p_lmu = lmu_g[idx];
     }
   };
 
@@ -305,7 +314,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         constexpr int i = decltype(I)::value;
         const int f = tid + i * NT;
         const bool is_y = f >= S::IN_TILE16;
-        if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && beh_lp)) {
+        if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
           const int g = is_y ? f - S::IN_TILE16 : f;
           const int r = g / S::IN_ROW16, c = g % S::IN_ROW16;
           lds[(is_y ? S::IN_LDS16 : 0) + r * S::IN_PITCH16 + c] = pre[i];
@@ -327,7 +336,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         if (te >= 0 && c < nb * A_) {
           const int64_t off = (te * B + b0) * A_ + c;
           lz[rr * S::IN_PITCH + c] = static_cast<const In*>(a.target_logits)[off];
-          if (!beh_lp) ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
+          if (!skip_y) ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
         }
       }
       act = 0;
@@ -337,7 +346,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         r32 = a.rewards[idx];
         g32 = a.discounts[idx];
         V32 = a.values[idx];
-        if (beh_lp) lmu = lmu_g[idx];
+        if (beh_lp && !no_ratio) lmu = lmu_g[idx];
       }
       __syncthreads();
     }
@@ -351,7 +360,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
     float e[A_];
-    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, lmu, e);
+    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
     const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
