@@ -570,17 +570,18 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
 
 bool tiled_supported(const StepArgs& a, LogitsType) { return a.A == 9 || a.A == 18; }
 
-// Lanes per workgroup: fp32 logits use the count whose [t, b0:b0+LANES, :] run
-// is 1152 bytes (nine 128-byte lines); bf16 logits keep 512-thread workgroups
-// (576- and 1152-byte runs), whose register budget avoids spills.
+// Lanes per workgroup: 16 (256 threads) for A = 9 keeps twice as many
+// workgroups in flight for mid-sized batches (a 4096-lane batch fills all 256
+// CUs); A = 18 uses 16 lanes for fp32 logits (1152-byte runs, nine 128-byte
+// lines) and 32 for bf16 logits.
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups) {
   if (lt == LogitsType::F32) {
     if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups);
-    if (a.A == 9) return launch_shape<9, 32, float>(a, mode, st, num_workgroups);
+    if (a.A == 9) return launch_shape<9, 16, float>(a, mode, st, num_workgroups);
   } else {
     if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups);
-    if (a.A == 9) return launch_shape<9, 32, uint16_t>(a, mode, st, num_workgroups);
+    if (a.A == 9) return launch_shape<9, 16, uint16_t>(a, mode, st, num_workgroups);
   }
   return hipErrorNotSupported;
 }
