@@ -275,3 +275,19 @@ def test_kernels_agree(monkeypatch, pidx):
         for name in ("lane_losses", "losses"):
             assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
                          np_out(getattr(b, name)))
+
+
+def test_offsets_beyond_two_gib():
+    """Logit tensors larger than 2^31 bytes (T=64, B=524288, A=18: 2.4 GB each):
+    byte offsets need 64 bits; the oracle checks lanes spread over the batch,
+    including the last ones."""
+    T, B, A = 64, 1 << 19, 18
+    log_case(f"large batch T={T} B={B} A={A} ({T * B * A * 4 / 2**30:.2f} GiB per logit tensor)")
+    tr = make_random(T, B, A, 4321, noise_std=1.0, end_prob=0.01)
+    dev = to_device(tr)
+    lanes = sorted(set([0, 1, B // 2, B - 17, B - 2, B - 1] + list(range(B - 64, B, 7))))
+    for p in (PARAM_SETS[4][0], PARAM_SETS[4][1]):
+        out = run_loss_grad(dev, p)
+        check_against_oracle(tr, p, out, lanes=lanes)
+    del dev
+    torch.cuda.empty_cache()
