@@ -24,3 +24,4 @@ from .definitions import (  # noqa: F401
     total_loss_frozen_targets,
     transform_rewards,
 )
+from .head import HeadOut, head_forward, head_loss_and_grads, sum_term_scale  # noqa: F401

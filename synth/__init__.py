@@ -16,3 +16,12 @@ from .trajectories import (  # noqa: F401
     make_random,
     subset_lanes,
 )
+from .head import (  # noqa: F401
+    HEAD_CONFIGS,
+    HeadBatch,
+    head_batch_from_device,
+    make_head,
+    make_head_config,
+    make_head_device,
+    subset_head_lanes,
+)

@@ -54,3 +54,22 @@ def test_subset_lanes():
     assert sub.B == 3
     assert np.array_equal(sub.target_logits[:, 1], tr.target_logits[:, 5])
     assert np.array_equal(sub.bootstrap_value, tr.bootstrap_value[[0, 5, 31]])
+
+
+def test_head_batches_are_seeded_and_shaped():
+    from synth import HEAD_CONFIGS, make_head, make_head_config, subset_head_lanes
+    a = make_head(9, 5, 7, 64, 42)
+    b = make_head(9, 5, 7, 64, 42)
+    for f in ("hidden_bits", "weight_bits", "bias", "behaviour_logits", "actions", "rewards",
+              "discounts", "bootstrap_value"):
+        np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
+    assert a.hidden_bits.shape == (9, 5, 64) and a.hidden_bits.dtype == np.uint16
+    assert a.weight_bits.shape == (64, 8) and a.bias.shape == (8,)
+    assert np.all(np.abs(a.hidden) <= 1.0)
+    assert a.actions.min() >= 0 and a.actions.max() < 7
+    assert set(np.unique(a.discounts)) <= {0.0, np.float32(0.99)}
+    c = make_head_config("atari")
+    assert (c.T, c.B, c.A, c.H) == (HEAD_CONFIGS["atari"]["T"], 32, 18, 256)
+    s = subset_head_lanes(c, [3, 0])
+    np.testing.assert_array_equal(s.hidden_bits[:, 1], c.hidden_bits[:, 0])
+    np.testing.assert_array_equal(s.bootstrap_value, c.bootstrap_value[[3, 0]])
