@@ -172,8 +172,8 @@ vtrace_status vtrace_targets(
  * The V-trace actor-critic losses and their gradients (Sec. 4.2), fused with the
  * targets into one pass over the batch.
  *
- * Losses, summed over batch and time (paper App. D: "the loss is summed across
- * the batch and time dimensions"):
+ * Losses, each a sum (not a mean) over batch and time, as the caption of the
+ * hyperparameter-range table in App. D states:
  *   policy gradient  L_pg  = -sum pg_adv_s * log pi(a_s|x_s)
  *   baseline         L_v   = baseline_cost * 1/2 * sum (v_s - V(x_s))^2
  *   entropy          L_ent = entropy_cost * sum_s sum_a pi(a|x_s) log pi(a|x_s)
@@ -243,6 +243,59 @@ vtrace_status vtrace_gather_logits(
     int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
     const void* target_logits, const void* behaviour_logits, const int32_t* actions,
     void* gathered, vtrace_stream_t stream);
+
+/*
+ * The learner's output layer fused with the V-trace losses and the gradients
+ * through the layer.  Sec. 3.1: after the LSTM, the fully connected output
+ * layer is applied to all time steps at once.  Here that layer maps each
+ * step's hidden state to A policy logits and the baseline,
+ *   o[t,b,:] = hidden[t,b,:] @ head_weight + head_bias,
+ *   policy logits = o[..., 0:A],  V(x_t) = o[..., A],
+ * and the call computes the losses of vtrace_loss_grad on (logits, V) and, with
+ * G = [d_logits, d_values] (dL/do),
+ *   d_hidden = G @ head_weight^T,
+ *   d_weight = sum over (t,b) of hidden[t,b,:]^T G[t,b,:],
+ *   d_bias   = sum over (t,b) of G[t,b,:].
+ * The logits, the values and their gradients never reach HBM.
+ *
+ *   H               hidden size: 64, 128 or 256 (else VTRACE_ERR_SHAPE)
+ *   A               1..31 actions (A + 1 outputs; else VTRACE_ERR_SHAPE)
+ *   behaviour_dtype element type of behaviour logits (VTRACE_F32 / VTRACE_BF16);
+ *                   with variant->behaviour_input == LOG_PROBS `behaviour` is
+ *                   [T,B] float32 log mu(a_t|x_t) and this is not used
+ *   hidden          [T,B,H] bfloat16, 16-byte aligned
+ *   head_weight     [H,A+1] bfloat16 (2-byte aligned), column A is the baseline
+ *   head_bias       [A+1] float32
+ *   behaviour       [T,B,A] behaviour logits (element-aligned) or log-probabilities
+ *   bootstrap_value [B] float32 V(x_T): a target, it receives no gradient
+ *   variant         as in vtrace_loss_grad_ex (NULL = V-trace); grad_dtype is
+ *                   the element type of d_hidden
+ *   losses          [4] float32, as in vtrace_loss_grad
+ *   d_hidden        [T,B,H] float32 or bfloat16, 16-byte aligned
+ *   d_weight        [H,A+1] float32;  d_bias [A+1] float32
+ *   vs, pg_advantages, lane_losses   optional, as in vtrace_loss_grad
+ *   outputs         optional [T,B,A+1] float32: the layer's outputs o
+ *   workspace       required, >= vtrace_head_workspace_bytes(T,B,A,H) bytes,
+ *                   16-byte aligned, cleared once by vtrace_workspace_init
+ * The products use bfloat16 inputs with float32 accumulation; G enters them as
+ * a bfloat16 pair (high part + low part, 2^-17 relative), so d_hidden keeps
+ * float32 accuracy.  d_weight, d_bias and the losses are reduced in a fixed
+ * order: repeated calls give bit-identical results.  An out-of-range action
+ * sets the workspace flag and makes d_weight and d_bias NaN, besides its own
+ * step's outputs.
+ */
+size_t vtrace_head_workspace_bytes(int64_t T, int64_t B, int64_t A, int64_t H);
+
+vtrace_status vtrace_head_loss_grad(
+    int64_t T, int64_t B, int64_t A, int64_t H, vtrace_dtype behaviour_dtype,
+    const void* hidden, const void* head_weight, const float* head_bias,
+    const void* behaviour, const int32_t* actions, const float* rewards,
+    const float* discounts, const float* bootstrap_value,
+    float rho_bar, float c_bar, float lambda, float baseline_cost, float entropy_cost,
+    const vtrace_variant* variant,
+    float* losses, void* d_hidden, float* d_weight, float* d_bias,
+    float* vs, float* pg_advantages, float* lane_losses, float* outputs,
+    void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
 
 /*
  * Synchronises `stream`, then reads the workspace's sticky out-of-range-action

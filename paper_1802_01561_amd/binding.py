@@ -16,11 +16,14 @@ from ._lib import (BEHAVIOUR_INPUTS, CORRECTIONS, Q_ESTIMATES, REWARD_TRANSFORMS
                    VTRACE_F32, Variant, check, lib)
 
 __all__ = [
+    "HeadLossGrad",
     "LossGrad",
     "Workspace",
     "vtrace_abi_version",
     "vtrace_error_flag",
     "vtrace_gather_logits",
+    "vtrace_head_loss_grad",
+    "vtrace_head_workspace_bytes",
     "vtrace_loss_grad",
     "vtrace_max_elements",
     "vtrace_targets",
@@ -102,19 +105,25 @@ def vtrace_workspace_bytes(T: int, B: int, A: int) -> int:
     return lib().vtrace_workspace_bytes(T, B, A)
 
 
-class Workspace:
-    """Device workspace for vtrace_loss_grad, cleared on creation."""
+def vtrace_head_workspace_bytes(T: int, B: int, A: int, H: int) -> int:
+    return lib().vtrace_head_workspace_bytes(T, B, A, H)
 
-    def __init__(self, T: int, B: int, A: int, device=None, stream=None):
-        n = vtrace_workspace_bytes(T, B, A)
+
+class Workspace:
+    """Device workspace for vtrace_loss_grad (or, with H, for
+    vtrace_head_loss_grad), cleared on creation."""
+
+    def __init__(self, T: int, B: int, A: int, device=None, stream=None, *, H: Optional[int] = None):
+        n = vtrace_workspace_bytes(T, B, A) if H is None else vtrace_head_workspace_bytes(T, B, A, H)
         if n == 0:
-            raise ValueError(f"invalid batch shape T={T} B={B} A={A}")
+            raise ValueError(f"invalid batch shape T={T} B={B} A={A} H={H}")
         self.nbytes = n
         self.tensor = torch.empty(n, dtype=torch.uint8, device=device or "cuda")
         check(lib().vtrace_workspace_init(_p(self.tensor), n, _stream(stream)))
 
-    def fits(self, T: int, B: int, A: int) -> bool:
-        return self.nbytes >= vtrace_workspace_bytes(T, B, A)
+    def fits(self, T: int, B: int, A: int, H: Optional[int] = None) -> bool:
+        need = vtrace_workspace_bytes(T, B, A) if H is None else vtrace_head_workspace_bytes(T, B, A, H)
+        return self.nbytes >= need
 
 
 class LossGrad(NamedTuple):
@@ -195,6 +204,80 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
         _p(out.d_values),
         _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses),
         _p(workspace.tensor), workspace.nbytes, _stream(stream)))
+    return out
+
+
+class HeadLossGrad(NamedTuple):
+    losses: torch.Tensor  # [4] total, policy gradient, baseline, entropy
+    d_hidden: torch.Tensor  # [T,B,H]
+    d_weight: torch.Tensor  # [H,A+1]
+    d_bias: torch.Tensor  # [A+1]
+    vs: Optional[torch.Tensor]
+    pg_advantages: Optional[torch.Tensor]
+    lane_losses: Optional[torch.Tensor]
+    outputs: Optional[torch.Tensor]  # [T,B,A+1] the layer's outputs
+
+
+def vtrace_head_loss_grad(hidden, head_weight, head_bias, behaviour_logits, actions, rewards,
+                          discounts, bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0,
+                          baseline_cost=0.5, entropy_cost=0.01, *,
+                          workspace: Optional[Workspace] = None, with_vs=False,
+                          with_pg_advantages=False, with_lane_losses=False, with_outputs=False,
+                          out: Optional[HeadLossGrad] = None, stream=None, correction="vtrace",
+                          q_estimate="vtrace", epsilon=1e-6, behaviour="logits",
+                          reward_transform=None, grad_dtype=torch.float32) -> HeadLossGrad:
+    """Output layer o = hidden @ head_weight + head_bias (policy logits, then the
+    baseline), the V-trace losses on it and the gradients through the layer.
+
+    hidden [T,B,H] and head_weight [H,A+1] are bfloat16; the variant arguments
+    are as in vtrace_loss_grad; ``grad_dtype`` is d_hidden's type."""
+    variant = _variant(correction, q_estimate, epsilon, behaviour, reward_transform, grad_dtype)
+    if hidden.dim() != 3 or head_weight.dim() != 2:
+        raise ValueError("hidden must be [T, B, H] and head_weight [H, A + 1]")
+    T, B, H = hidden.shape
+    A = head_weight.shape[1] - 1
+    dev = hidden.device
+    if dev.type != "cuda":
+        raise ValueError("inputs must be on a GPU device")
+    _require(hidden, "hidden", (T, B, H), torch.bfloat16, dev)
+    _require(head_weight, "head_weight", (H, A + 1), torch.bfloat16, dev)
+    _require(head_bias, "head_bias", (A + 1,), torch.float32, dev)
+    if behaviour == "log_probs":
+        _require(behaviour_logits, "behaviour log-probabilities", (T, B), torch.float32, dev)
+        code = VTRACE_F32
+    else:
+        _require(behaviour_logits, "behaviour_logits", (T, B, A), None, dev)
+        code = _dtype_code(behaviour_logits)
+    _require(actions, "actions", (T, B), torch.int32, dev)
+    for name, t in (("rewards", rewards), ("discounts", discounts)):
+        _require(t, name, (T, B), torch.float32, dev)
+    _require(bootstrap_value, "bootstrap_value", (B,), torch.float32, dev)
+    if workspace is None:
+        workspace = Workspace(T, B, A, device=dev, stream=stream, H=H)
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        out = HeadLossGrad(
+            torch.empty(4, **f32), torch.empty((T, B, H), dtype=grad_dtype, device=dev),
+            torch.empty((H, A + 1), **f32), torch.empty(A + 1, **f32),
+            torch.empty((T, B), **f32) if with_vs else None,
+            torch.empty((T, B), **f32) if with_pg_advantages else None,
+            torch.empty((B, 3), **f32) if with_lane_losses else None,
+            torch.empty((T, B, A + 1), **f32) if with_outputs else None)
+    _require(out.losses, "losses", (4,), torch.float32, dev)
+    _require(out.d_hidden, "d_hidden", (T, B, H), grad_dtype, dev)
+    _require(out.d_weight, "d_weight", (H, A + 1), torch.float32, dev)
+    _require(out.d_bias, "d_bias", (A + 1,), torch.float32, dev)
+    for name, t, shape in (("vs", out.vs, (T, B)), ("pg_advantages", out.pg_advantages, (T, B)),
+                           ("lane_losses", out.lane_losses, (B, 3)),
+                           ("outputs", out.outputs, (T, B, A + 1))):
+        if t is not None:
+            _require(t, name, shape, torch.float32, dev)
+    check(lib().vtrace_head_loss_grad(
+        T, B, A, H, code, _p(hidden), _p(head_weight), _p(head_bias), _p(behaviour_logits),
+        _p(actions), _p(rewards), _p(discounts), _p(bootstrap_value), rho_bar, c_bar, lam,
+        baseline_cost, entropy_cost, ctypes.byref(variant), _p(out.losses), _p(out.d_hidden),
+        _p(out.d_weight), _p(out.d_bias), _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses),
+        _p(out.outputs), _p(workspace.tensor), workspace.nbytes, _stream(stream)))
     return out
 
 

@@ -96,15 +96,19 @@ void attach_workspace(StepArgs* a, void* ws) {
   a->partials = reinterpret_cast<double*>(base + vtrace::kWsHeaderBytes);
 }
 
-// Copies a caller's variant into the launch arguments (NULL = V-trace).
-vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
-  a->correction = VTRACE_CORRECTION_VTRACE;
-  a->q_estimate = VTRACE_Q_VTRACE;
-  a->epsilon = 0.0f;
-  a->behaviour_log_probs = 0;
-  a->reward_transform = VTRACE_REWARD_RAW;
-  a->grad_bf16 = 0;
-  if (v == nullptr) return aligned(a->behaviour_logits, 16) ? VTRACE_OK : VTRACE_ERR_ALIGN;
+// A caller's variant, checked (NULL = V-trace with float32 gradients).
+struct Variant {
+  int correction = VTRACE_CORRECTION_VTRACE;
+  int q_estimate = VTRACE_Q_VTRACE;
+  float epsilon = 0.0f;
+  int behaviour_log_probs = 0;
+  int reward_transform = VTRACE_REWARD_RAW;
+  int grad_bf16 = 0;
+};
+
+vtrace_status parse_variant(const vtrace_variant* v, Variant* out) {
+  *out = Variant{};
+  if (v == nullptr) return VTRACE_OK;
   if (v->correction < VTRACE_CORRECTION_VTRACE || v->correction > VTRACE_CORRECTION_ONE_STEP_IS)
     return VTRACE_ERR_PARAM;
   if (v->q_estimate != VTRACE_Q_VTRACE && v->q_estimate != VTRACE_Q_BASELINE) return VTRACE_ERR_PARAM;
@@ -115,16 +119,35 @@ vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
   if (v->reward_transform < VTRACE_REWARD_RAW || v->reward_transform > VTRACE_REWARD_ASYMMETRIC)
     return VTRACE_ERR_PARAM;
   if (v->grad_dtype != VTRACE_F32 && v->grad_dtype != VTRACE_BF16) return VTRACE_ERR_DTYPE;
-  // Logit rows are read with 16-byte vectors; log-probabilities are plain floats.
-  if (v->behaviour_input == VTRACE_BEHAVIOUR_LOGITS && !aligned(a->behaviour_logits, 16))
-    return VTRACE_ERR_ALIGN;
-  a->correction = v->correction;
-  a->q_estimate = v->q_estimate;
-  a->epsilon = v->epsilon;
-  a->behaviour_log_probs = v->behaviour_input == VTRACE_BEHAVIOUR_LOG_PROBS;
-  a->reward_transform = v->reward_transform;
-  a->grad_bf16 = v->grad_dtype == VTRACE_BF16;
+  out->correction = v->correction;
+  out->q_estimate = v->q_estimate;
+  out->epsilon = v->epsilon;
+  out->behaviour_log_probs = v->behaviour_input == VTRACE_BEHAVIOUR_LOG_PROBS;
+  out->reward_transform = v->reward_transform;
+  out->grad_bf16 = v->grad_dtype == VTRACE_BF16;
   return VTRACE_OK;
+}
+
+// Copies a caller's variant into the launch arguments.
+vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
+  Variant f;
+  const vtrace_status st = parse_variant(v, &f);
+  if (st != VTRACE_OK) return st;
+  // Logit rows are read with 16-byte vectors; log-probabilities are plain floats.
+  if (!f.behaviour_log_probs && !aligned(a->behaviour_logits, 16)) return VTRACE_ERR_ALIGN;
+  a->correction = f.correction;
+  a->q_estimate = f.q_estimate;
+  a->epsilon = f.epsilon;
+  a->behaviour_log_probs = f.behaviour_log_probs;
+  a->reward_transform = f.reward_transform;
+  a->grad_bf16 = f.grad_bf16;
+  return VTRACE_OK;
+}
+
+bool head_shape_ok(int64_t T, int64_t B, int64_t A, int64_t H) {
+  return A >= 1 && A <= vtrace::kHeadMaxActions && vtrace::head_hidden_supported(H) &&
+         shape_ok(T, B, H) &&
+         shape_ok(T, B, A + 1);
 }
 
 vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s) {
@@ -148,13 +171,17 @@ const char* vtrace_status_string(vtrace_status s) {
   switch (s) {
     case VTRACE_OK: return "ok";
     case VTRACE_ERR_NULL: return "a required pointer is NULL";
-    case VTRACE_ERR_SHAPE: return "T, B and A must be >= 1 and T*B*A within vtrace_max_elements()";
+    case VTRACE_ERR_SHAPE:
+      return "T, B and A must be >= 1 and T*B*A within vtrace_max_elements(); the fused output "
+             "layer also needs A <= 31 and H in {64, 128, 256}";
     case VTRACE_ERR_DTYPE: return "unknown logits dtype";
     case VTRACE_ERR_PARAM:
       return "bad parameter: rho_bar, c_bar must be >= 0 (inf allowed), lambda in [0,1], "
              "costs finite, none NaN; a variant needs a known correction and Q estimate and, "
              "for epsilon-correction, a finite epsilon > 0";
-    case VTRACE_ERR_ALIGN: return "misaligned pointer: logits/d_logits/gathered need 16 bytes, others 4";
+    case VTRACE_ERR_ALIGN:
+      return "misaligned pointer: logits/d_logits/gathered/hidden/d_hidden need 16 bytes, "
+             "others their element size";
     case VTRACE_ERR_WORKSPACE: return "workspace missing or smaller than vtrace_workspace_bytes()";
     case VTRACE_ERR_HIP: return "the HIP runtime rejected the kernel launch";
   }
@@ -290,6 +317,83 @@ vtrace_status vtrace_gather_logits(int64_t T, int64_t B, int64_t A, vtrace_dtype
                                as_hip(stream)) == hipSuccess
              ? VTRACE_OK
              : VTRACE_ERR_HIP;
+}
+
+size_t vtrace_head_workspace_bytes(int64_t T, int64_t B, int64_t A, int64_t H) {
+  if (!head_shape_ok(T, B, A, H)) return 0;
+  return vtrace::head_workspace_bytes(B, A, H);
+}
+
+vtrace_status vtrace_head_loss_grad(
+    int64_t T, int64_t B, int64_t A, int64_t H, vtrace_dtype behaviour_dtype, const void* hidden,
+    const void* head_weight, const float* head_bias, const void* behaviour, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* bootstrap_value, float rho_bar,
+    float c_bar, float lambda, float baseline_cost, float entropy_cost,
+    const vtrace_variant* variant, float* losses, void* d_hidden, float* d_weight, float* d_bias,
+    float* vs, float* pg_advantages, float* lane_losses, float* outputs, void* workspace,
+    size_t workspace_bytes, vtrace_stream_t stream) {
+  if (!hidden || !head_weight || !head_bias || !behaviour || !actions || !rewards || !discounts ||
+      !bootstrap_value || !losses || !d_hidden || !d_weight || !d_bias)
+    return VTRACE_ERR_NULL;
+  if (!head_shape_ok(T, B, A, H)) return VTRACE_ERR_SHAPE;
+  LogitsType lt;
+  if (!dtype_of(behaviour_dtype, &lt)) return VTRACE_ERR_DTYPE;
+  if (!truncation_ok(rho_bar) || !truncation_ok(c_bar)) return VTRACE_ERR_PARAM;
+  if (std::isnan(lambda) || lambda < 0.0f || lambda > 1.0f) return VTRACE_ERR_PARAM;
+  if (!std::isfinite(baseline_cost) || !std::isfinite(entropy_cost)) return VTRACE_ERR_PARAM;
+  Variant f;
+  vtrace_status st = parse_variant(variant, &f);
+  if (st != VTRACE_OK) return st;
+  const uintptr_t beh_align = (f.behaviour_log_probs || lt == LogitsType::F32) ? 4 : 2;
+  if (!aligned(hidden, 16) || !aligned(d_hidden, 16) || !aligned(head_weight, 2) ||
+      !aligned(behaviour, beh_align))
+    return VTRACE_ERR_ALIGN;
+  if (!aligned(head_bias, 4) || !aligned(actions, 4) || !aligned(rewards, 4) ||
+      !aligned(discounts, 4) || !aligned(bootstrap_value, 4) || !aligned(losses, 4) ||
+      !aligned(d_weight, 4) || !aligned(d_bias, 4) || !aligned(vs, 4) ||
+      !aligned(pg_advantages, 4) || !aligned(lane_losses, 4) || !aligned(outputs, 4))
+    return VTRACE_ERR_ALIGN;
+  if (!workspace) return VTRACE_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
+  if (workspace_bytes < vtrace::head_workspace_bytes(B, A, H)) return VTRACE_ERR_WORKSPACE;
+
+  vtrace::HeadArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.T = T;
+  a.B = B;
+  a.A = A;
+  a.H = H;
+  a.hidden = static_cast<const uint16_t*>(hidden);
+  a.weight = static_cast<const uint16_t*>(head_weight);
+  a.bias = head_bias;
+  a.behaviour = behaviour;
+  a.actions = actions;
+  a.rewards = rewards;
+  a.discounts = discounts;
+  a.bootstrap_value = bootstrap_value;
+  a.rho_bar = rho_bar;
+  a.c_bar = c_bar;
+  a.lambda = lambda;
+  a.baseline_cost = baseline_cost;
+  a.entropy_cost = entropy_cost;
+  a.correction = f.correction;
+  a.q_estimate = f.q_estimate;
+  a.epsilon = f.epsilon;
+  a.behaviour_log_probs = f.behaviour_log_probs;
+  a.behaviour_bf16 = !f.behaviour_log_probs && lt == LogitsType::BF16;
+  a.reward_transform = f.reward_transform;
+  a.grad_bf16 = f.grad_bf16;
+  a.losses = losses;
+  a.d_hidden = d_hidden;
+  a.d_weight = d_weight;
+  a.d_bias = d_bias;
+  a.vs = vs;
+  a.pg_adv = pg_advantages;
+  a.lane_losses = lane_losses;
+  a.outputs = outputs;
+  vtrace::head_attach_workspace(&a, workspace);
+  (void)hipGetLastError();
+  return vtrace::launch_head(a, as_hip(stream)) == hipSuccess ? VTRACE_OK : VTRACE_ERR_HIP;
 }
 
 vtrace_status vtrace_error_flag(const void* workspace, int32_t* flag, vtrace_stream_t stream) {

@@ -1,0 +1,696 @@
+// Fused output layer + V-trace kernel.
+//
+// The learner applies its fully connected output layer to every step of the
+// unroll at once (Sec. 3.1): o = hidden @ W + bias with W: [H, A + 1], whose
+// first A outputs are the policy logits and whose last is the baseline V(x_t).
+// This kernel runs that layer, the V-trace targets, losses and gradients of
+// Sec. 4 on its outputs, and the gradients through the layer, in one pass over
+// HBM.  With G = dL/do = [d_logits, d_values]:
+//   d_hidden = G W^T,   d_W = sum over (t, b) of hidden^T G,   d_bias = sum of G.
+// The three products are dense contractions and run on the matrix cores
+// (bfloat16 operands, float32 accumulation).
+//
+// Work split.  A workgroup has four waves; wave w walks one lane (batch entry)
+// backwards in time in chunks of 16 steps, so the reverse recursion stays in
+// the wave, and workgroups loop over groups of four consecutive lanes.  In a
+// chunk the 16 steps of the wave's lane are the 16 rows of one MFMA tile; lane
+// l of the wave is (s, g) = (l % 16, l / 16).
+//  1. Forward, o^T = W^T hidden^T with 16x16x32 MFMAs (M: output column, N:
+//     step, K: hidden unit).  Lane (s, g) loads the K slice [g H/4, (g+1) H/4)
+//     of step s's hidden row as whole 16-byte vectors and receives o[s][4g + i]
+//     (and o[s][16 + 4g + i] when A + 1 > 16), i = 0..3.
+//  2. The V-trace epilogue works in that layout.  Row statistics of a step
+//     (maxima, exponent sums, the taken action's logit, the baseline) are sums
+//     over the four lane groups: two xor shuffles, whose fixed order gives all
+//     four groups bit-identical results.  The per-step chain and the suffix
+//     scan over the 16 steps then run on each DPP row of 16 lanes; the four
+//     rows compute the same values.
+//  3. d_hidden^T = W G^T (K: output column).  Each lane's G values are exactly
+//     the K slots it must supply, taking the forward's output order as the
+//     contraction order, so G enters the MFMA where the epilogue left it.  G
+//     is split into bfloat16 high and low parts (hi + lo equals G to within
+//     2^-17 relative), two MFMAs, so the product keeps float32 accuracy.  The
+//     M rows (hidden units) are ordered so that each lane receives H/4
+//     consecutive units of its step's row: whole 16-byte stores.
+//  4. d_W contracts over steps, which lie across lanes: the hidden tile and G
+//     are written to LDS, and after a workgroup barrier wave w accumulates
+//     rows [w H/4, (w+1) H/4) of d_W over the four lanes' tiles with 16x16x16
+//     MFMAs, in registers, for the whole walk (wave 0 also d_bias, with a ones
+//     operand).  A second kernel adds the workgroups' partial sums.
+#include "device_common.hpp"
+#include "wave_ops.hpp"
+
+namespace vtrace {
+namespace {
+
+constexpr int kL = 16;            // steps per chunk
+constexpr int kHeadWaves = 4;     // lanes in flight per workgroup
+constexpr int kHeadThreads = kHeadWaves * kWave;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+template <int H, int NT>
+struct HeadShape {
+  static constexpr int C = 16 * NT;     // output columns covered by the MFMA tiles
+  static constexpr int Q = H / 4;       // hidden units per lane group
+  static constexpr int KS = H / 32;     // forward K steps = 16-byte vectors per lane and row
+  static constexpr int MT = H / 16;     // d_hidden M tiles
+  static constexpr int MW = H / 64;     // d_W M tiles per wave
+  static constexpr int KW = 4 * NT;     // K slots per lane in the d_hidden product
+  // LDS row pitches in bfloat16 elements.  W^T rows are 16-byte aligned for
+  // the forward's vector reads; the hidden and G rows are 8-byte aligned and
+  // padded so that the four lane groups of a transposed read (rows 4 apart)
+  // fall on different banks.
+  static constexpr int WT_PITCH = H + 8;
+  static constexpr int WP_PITCH = (NT == 2) ? 40 : 20;
+  static constexpr int HL_PITCH = H + 4;
+  static constexpr int GL_PITCH = C + 4;
+  static_assert(H % 64 == 0 && H <= 256, "hidden size");
+  static_assert(NT == 1 || NT == 2, "column tiles");
+};
+
+// K slot of column c in the d_hidden product: the order in which the forward
+// product leaves a lane's outputs (columns 4g..4g+3, then 16+4g..16+4g+3).
+template <int NT>
+__device__ __forceinline__ int slot_of_column(int c) {
+  if constexpr (NT == 1) return c;
+  const int hi = c >= 16;
+  const int cc = c - 16 * hi;
+  return 8 * (cc / 4) + 4 * hi + (cc % 4);
+}
+
+__device__ __forceinline__ float group_sum(float v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+__device__ __forceinline__ double group_sum(double v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+__device__ __forceinline__ float group_max(float v) {
+  v = fmaxf(v, __shfl_xor(v, 16));
+  v = fmaxf(v, __shfl_xor(v, 32));
+  return v;
+}
+
+__device__ __forceinline__ f32x4 mfma_k32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_k16(s16x4 a, s16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+template <typename BehIn>
+__device__ __forceinline__ float load_behaviour(const void* p, int64_t i) {
+  return logit_to_float(static_cast<const BehIn*>(p)[i]);
+}
+
+template <int H, int NT, bool kPrecise, typename BehIn>
+__global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
+  using S = HeadShape<H, NT>;
+  constexpr int C = S::C, Q = S::Q;
+  __shared__ __align__(16) uint16_t s_wt[C * S::WT_PITCH];        // W^T [C][H]
+  __shared__ __align__(16) uint16_t s_wp[H * S::WP_PITCH];        // W [H][K slot]
+  __shared__ __align__(16) uint16_t s_h[kHeadWaves * kL * S::HL_PITCH];  // hidden tiles
+  __shared__ __align__(16) uint16_t s_ghi[kHeadWaves * kL * S::GL_PITCH];
+  __shared__ __align__(16) uint16_t s_glo[kHeadWaves * kL * S::GL_PITCH];
+  __shared__ double s_red[3 * kHeadWaves];
+
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int l = tid % kWave;
+  const int s = l % kL;  // step within the chunk (and row of MFMA operands)
+  const int g = l / kL;  // lane group
+  const int64_t T = a.T, B = a.B, A = a.A;
+  const int A1 = static_cast<int>(A) + 1;
+
+  // The layer's weights, twice: W^T for the forward, W in K-slot order for
+  // d_hidden.  Columns beyond the baseline are zero.
+  for (int i = tid; i < H * C; i += kHeadThreads) {
+    const int h = i / C, c = i % C;
+    const uint16_t v = c < A1 ? a.weight[static_cast<int64_t>(h) * A1 + c] : uint16_t(0);
+    s_wt[c * S::WT_PITCH + h] = v;
+    s_wp[h * S::WP_PITCH + slot_of_column<NT>(c)] = v;
+  }
+  float bias[NT][4];
+  static_for<NT>([&](auto CT) {
+    constexpr int ct = decltype(CT)::value;
+    for (int i = 0; i < 4; ++i) {
+      const int c = 16 * ct + 4 * g + i;
+      bias[ct][i] = c < A1 ? a.bias[c] : 0.0f;
+    }
+  });
+  __syncthreads();
+
+  const bool beh_lp = a.behaviour_log_probs != 0;
+  const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
+  const bool use_y = !beh_lp && !no_ratio;
+  const bool grad_bf16 = a.grad_bf16 != 0;
+  const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
+  const float ce = a.entropy_cost;
+  const int nchunks = static_cast<int>((T + kL - 1) / kL);
+  const int64_t nquads = (B + kHeadWaves - 1) / kHeadWaves;
+
+  f32x4 acc_w[S::MW][NT];
+  f32x4 acc_b[NT];
+  static_for<NT>([&](auto CT) {
+    constexpr int ct = decltype(CT)::value;
+    acc_b[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    static_for<S::MW>([&](auto MI) { acc_w[decltype(MI)::value][ct] = f32x4{0.f, 0.f, 0.f, 0.f}; });
+  });
+  double wave_pg = 0.0, wave_base = 0.0, wave_ent = 0.0;
+
+  for (int64_t quad = xcd_tile(blockIdx.x, gridDim.x); quad < nquads; quad += gridDim.x) {
+    const int64_t b = quad * kHeadWaves + w;
+    const bool lane_ok = b < B;
+    const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
+    double cy_V = boot, cy_v = boot, cy_A = 0.0;
+    double l_pg = 0.0, l_base = 0.0, l_ent = 0.0;
+
+    // Register prefetch of one chunk: this lane's hidden slice, behaviour
+    // values and per-step scalars.
+    v4u hreg[S::KS];
+    float yreg[NT][4];
+    int32_t p_act = 0;
+    float p_r = 0.f, p_g = 0.f, p_lmu = 0.f;
+    auto prefetch = [&](int k) {
+      int64_t t = T - static_cast<int64_t>(k + 1) * kL + s;
+      t = t < 0 ? 0 : t;  // rows before t = 0 reread row 0 and are masked later
+      const int64_t row = t * B + (lane_ok ? b : 0);
+      const v4u* hp = reinterpret_cast<const v4u*>(a.hidden + row * H + g * Q);
+      static_for<S::KS>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        hreg[j] = lane_ok ? __builtin_nontemporal_load(hp + j) : v4u{0u, 0u, 0u, 0u};
+      });
+      if (lane_ok) {
+        p_act = a.actions[row];
+        p_r = a.rewards[row];
+        p_g = a.discounts[row];
+        if (beh_lp && !no_ratio) p_lmu = static_cast<const float*>(a.behaviour)[row];
+      }
+      static_for<NT>([&](auto CT) {
+        constexpr int ct = decltype(CT)::value;
+        for (int i = 0; i < 4; ++i) {
+          const int c = 16 * ct + 4 * g + i;
+          yreg[ct][i] = (use_y && lane_ok && c < A) ? load_behaviour<BehIn>(a.behaviour, row * A + c) : 0.f;
+        }
+      });
+    };
+
+    prefetch(0);
+    for (int k = 0; k < nchunks; ++k) {
+      const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+      const int64_t t = t0 + s;
+      const bool step_ok = lane_ok && t >= 0;
+      const int64_t row = t * B + b;
+
+      // 1. Forward product, from the prefetched hidden slice.
+      f32x4 oacc[NT];
+      static_for<NT>([&](auto CT) { oacc[decltype(CT)::value] = f32x4{0.f, 0.f, 0.f, 0.f}; });
+      static_for<S::KS>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        const bf16x8 hv = __builtin_bit_cast(bf16x8, hreg[j]);
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          const bf16x8 wv =
+              *reinterpret_cast<const bf16x8*>(&s_wt[(16 * ct + s) * S::WT_PITCH + g * Q + 8 * j]);
+          oacc[ct] = mfma_k32(wv, hv, oacc[ct]);
+        });
+      });
+      // The hidden slice goes to LDS for d_W (the previous chunk's readers
+      // finished at its closing barrier).
+      {
+        uint16_t* hrow = s_h + (kL * w + s) * S::HL_PITCH + g * Q;
+        static_for<S::KS>([&](auto J) {
+          constexpr int j = decltype(J)::value;
+          reinterpret_cast<uint2*>(hrow + 8 * j)[0] = uint2{hreg[j].x, hreg[j].y};
+          reinterpret_cast<uint2*>(hrow + 8 * j)[1] = uint2{hreg[j].z, hreg[j].w};
+        });
+      }
+      int32_t act = p_act;
+      float r32 = p_r, g32 = p_g;
+      const float lmu = p_lmu;
+      float y[NT][4];
+      static_for<NT>([&](auto CT) {
+        constexpr int ct = decltype(CT)::value;
+        for (int i = 0; i < 4; ++i) y[ct][i] = yreg[ct][i];
+      });
+      if (k + 1 < nchunks) prefetch(k + 1);
+
+      // 2. Epilogue.
+      r32 = transform_reward(r32, a.reward_transform);
+      if (!step_ok) act = 0;
+      const bool act_ok = act >= 0 && act < A;
+      const int act_c = act_ok ? act : 0;
+      if (!act_ok) raise_error_flag(a.error_flag);
+
+      float o[NT][4];
+      float zmax = -INFINITY, ymax = -INFINITY, vloc = 0.f, zaloc = 0.f, yaloc = 0.f;
+      static_for<NT>([&](auto CT) {
+        constexpr int ct = decltype(CT)::value;
+        for (int i = 0; i < 4; ++i) {
+          const int c = 16 * ct + 4 * g + i;
+          o[ct][i] = oacc[ct][i] + bias[ct][i];
+          if (c < A) {
+            zmax = fmaxf(zmax, o[ct][i]);
+            ymax = fmaxf(ymax, y[ct][i]);
+          }
+          if (c == A) vloc = o[ct][i];
+          if (c == act_c) {
+            zaloc = o[ct][i];
+            yaloc = y[ct][i];
+          }
+        }
+      });
+      if (a.outputs != nullptr && step_ok) {
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          for (int i = 0; i < 4; ++i) {
+            const int c = 16 * ct + 4 * g + i;
+            if (c < A1) a.outputs[row * A1 + c] = o[ct][i];
+          }
+        });
+      }
+      const float V32 = group_sum(vloc);
+      const float mz = group_max(zmax);
+      const float za = group_sum(zaloc);
+
+      float e[NT][4];
+      double ratio;
+      float inv_s, log_s, one_minus_pa, e_a, ed;
+      if constexpr (kPrecise) {
+        double szl = 0.0, syl = 0.0;
+        float edl = 0.f;
+        const float my = use_y ? group_max(ymax) : 0.f;
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          for (int i = 0; i < 4; ++i) {
+            const int c = 16 * ct + 4 * g + i;
+            e[ct][i] = 0.f;
+            if (c < A) {
+              const double d = static_cast<double>(o[ct][i]) - static_cast<double>(mz);
+              const double x = exp_nonpos_f64(d);
+              szl += x;
+              e[ct][i] = static_cast<float>(x);
+              edl = fmaf(e[ct][i], static_cast<float>(d), edl);
+              if (use_y) syl += exp_nonpos_f64(static_cast<double>(y[ct][i]) - static_cast<double>(my));
+            }
+          }
+        });
+        const double sz = group_sum(szl);
+        ed = group_sum(edl);
+        const double inv = 1.0 / sz;
+        const double dza = static_cast<double>(za) - static_cast<double>(mz);
+        const double ea = exp_nonpos_f64(dza);
+        if (no_ratio) {
+          ratio = act_ok ? 1.0 : NAN;
+        } else if (beh_lp) {
+          ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
+        } else {
+          const double sy = group_sum(syl);
+          const double ya = static_cast<double>(group_sum(yaloc));
+          ratio = act_ok ? exp(dza - (ya - static_cast<double>(my))) * (sy * inv) : NAN;
+        }
+        inv_s = static_cast<float>(inv);
+        log_s = static_cast<float>(log(sz));
+        one_minus_pa = static_cast<float>((sz - ea) * inv);
+        e_a = static_cast<float>(ea);
+      } else {
+        float szl = 0.f, syl = 0.f, edl = 0.f;
+        const float my = use_y ? group_max(ymax) : 0.f;
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          for (int i = 0; i < 4; ++i) {
+            const int c = 16 * ct + 4 * g + i;
+            e[ct][i] = 0.f;
+            if (c < A) {
+              const float d = o[ct][i] - mz;
+              e[ct][i] = exp_fast(d);
+              szl += e[ct][i];
+              edl = fmaf(e[ct][i], d, edl);
+              if (use_y) syl += exp_fast(y[ct][i] - my);
+            }
+          }
+        });
+        const float sz = group_sum(szl);
+        ed = group_sum(edl);
+        const float inv = __builtin_amdgcn_rcpf(sz);
+        const float ea = exp_fast(za - mz);
+        log_s = __logf(sz);
+        if (no_ratio) {
+          ratio = act_ok ? 1.0 : NAN;
+        } else if (beh_lp) {
+          ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - log_s - lmu)) : NAN;
+        } else {
+          const float sy = group_sum(syl);
+          const float ya = group_sum(yaloc);
+          ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
+        }
+        inv_s = inv;
+        one_minus_pa = (sz - ea) * inv;
+        e_a = ea;
+      }
+      const float Hent = log_s - ed * inv_s;  // entropy of pi at this step
+
+      const StepWeights wts = variant_weights(a.correction, clip_above(ratio, rho_bar),
+                                              lam * clip_above(ratio, c_bar), lam, act_ok);
+      const double r = r32, gm = g32, V = V32;
+      double V_next = dpp_f64<kRowShl1>(V);
+      if (s == kL - 1) V_next = cy_V;
+      const double delta = wts.rho_v * (r + gm * V_next - V);
+      // Suffix scan of the affine maps v_t - V_t = delta_t + gamma_t c_t (v_{t+1} - V_{t+1})
+      // (Remark 1) over the row, the later chunk's carry folded into step 15.
+      double Gs = gm * wts.c_v, D = delta;
+      if (s == kL - 1) D = fma(Gs, cy_A, D);
+      static_for<4>([&](auto I) {
+        constexpr int off = 1 << decltype(I)::value;
+        const double Gn = dpp_f64<0x100 + off>(Gs);
+        const double Dn = dpp_f64<0x100 + off>(D);
+        if (s + off < kL) {
+          D = fma(Gs, Dn, D);
+          Gs = Gs * Gn;
+        }
+      });
+      const double A_t = D;
+      const double v_t = V + A_t;
+      double v_next = dpp_f64<kRowShl1>(v_t);
+      if (s == kL - 1) v_next = cy_v;
+      const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+      const double adv = wts.rho_pg * (r + gm * q_next - V);
+      cy_A = dpp_f64<kRowShr15>(A_t);
+      cy_v = dpp_f64<kRowShr15>(v_t);
+      cy_V = dpp_f64<kRowShr15>(V);
+
+      if (step_ok && g == 0) {
+        if (a.vs) a.vs[row] = static_cast<float>(v_t);
+        if (a.pg_adv) a.pg_adv[row] = static_cast<float>(adv);
+      }
+
+      // G = dL/do for this step: the policy-logit gradient of the plain loss
+      // (e_j (alpha + beta z_j) off the taken action), then d_values.
+      const float Kz = mz + log_s - Hent;
+      const float pa = e_a * inv_s;
+      const bool eps_mode = a.correction == kCorrEpsilon;
+      const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
+      const float adv32 = static_cast<float>(adv) * pg_w;
+      const float beta = inv_s * ce;
+      const float alpha = inv_s * adv32 - beta * Kz;
+      const float out_a = -adv32 * one_minus_pa + ce * pa * (za - Kz);
+      const float dval = static_cast<float>(a.baseline_cost * (V - v_t));
+      float Gv[NT][4];
+      static_for<NT>([&](auto CT) {
+        constexpr int ct = decltype(CT)::value;
+        for (int i = 0; i < 4; ++i) {
+          const int c = 16 * ct + 4 * g + i;
+          float x = 0.f;
+          if (c < A) x = (c == act_c) ? (act_ok ? out_a : NAN) : e[ct][i] * fmaf(beta, o[ct][i], alpha);
+          if (c == A) x = dval;
+          Gv[ct][i] = step_ok ? x : 0.f;
+        }
+      });
+      if (step_ok && g == 0) {
+        const double log_pa =
+            !act_ok ? NAN
+            : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
+                       : static_cast<double>(za - mz) - static_cast<double>(log_s);
+        l_pg += -adv * log_pa;
+        l_base += 0.5 * A_t * A_t;
+        l_ent += -static_cast<double>(Hent);
+      }
+
+      // 3. d_hidden = G W^T.
+      const int grow = (kL * w + s) * S::GL_PITCH;
+      if constexpr (NT == 2) {
+        const f32x8 gf = {Gv[0][0], Gv[0][1], Gv[0][2], Gv[0][3],
+                          Gv[1][0], Gv[1][1], Gv[1][2], Gv[1][3]};
+        const bf16x8 ghi = __builtin_convertvector(gf, bf16x8);
+        const bf16x8 glo = __builtin_convertvector(gf - __builtin_convertvector(ghi, f32x8), bf16x8);
+        const v4u uhi = __builtin_bit_cast(v4u, ghi), ulo = __builtin_bit_cast(v4u, glo);
+        reinterpret_cast<uint2*>(s_ghi + grow + 4 * g)[0] = uint2{uhi.x, uhi.y};
+        reinterpret_cast<uint2*>(s_ghi + grow + 16 + 4 * g)[0] = uint2{uhi.z, uhi.w};
+        reinterpret_cast<uint2*>(s_glo + grow + 4 * g)[0] = uint2{ulo.x, ulo.y};
+        reinterpret_cast<uint2*>(s_glo + grow + 16 + 4 * g)[0] = uint2{ulo.z, ulo.w};
+        f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+        static_for<S::MT>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          const int hrow = (s / 4) * Q + 4 * i + (s % 4);
+          const bf16x8 wv = *reinterpret_cast<const bf16x8*>(&s_wp[hrow * S::WP_PITCH + 8 * g]);
+          f32x4 acc = mfma_k32(wv, ghi, f32x4{0.f, 0.f, 0.f, 0.f});
+          acc = mfma_k32(wv, glo, acc);
+          if (step_ok) {
+            if (!grad_bf16) {
+              __builtin_nontemporal_store(
+                  acc, reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + g * Q + 4 * i));
+            } else if (i % 2 == 1) {
+              const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
+                              pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+              __builtin_nontemporal_store(
+                  pk, reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + g * Q + 4 * (i - 1)));
+            }
+          }
+          prev = acc;
+        });
+      } else {
+        const f32x4 gf = {Gv[0][0], Gv[0][1], Gv[0][2], Gv[0][3]};
+        const bf16x4 ghi = __builtin_convertvector(gf, bf16x4);
+        const bf16x4 glo = __builtin_convertvector(gf - __builtin_convertvector(ghi, f32x4), bf16x4);
+        const s16x4 shi = __builtin_bit_cast(s16x4, ghi), slo = __builtin_bit_cast(s16x4, glo);
+        reinterpret_cast<s16x4*>(s_ghi + grow + 4 * g)[0] = shi;
+        reinterpret_cast<s16x4*>(s_glo + grow + 4 * g)[0] = slo;
+        f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+        static_for<S::MT>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          const int hrow = (s / 4) * Q + 4 * i + (s % 4);
+          const s16x4 wv = *reinterpret_cast<const s16x4*>(&s_wp[hrow * S::WP_PITCH + 4 * g]);
+          f32x4 acc = mfma_k16(wv, shi, f32x4{0.f, 0.f, 0.f, 0.f});
+          acc = mfma_k16(wv, slo, acc);
+          if (step_ok) {
+            if (!grad_bf16) {
+              __builtin_nontemporal_store(
+                  acc, reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + g * Q + 4 * i));
+            } else if (i % 2 == 1) {
+              const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
+                              pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+              __builtin_nontemporal_store(
+                  pk, reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + g * Q + 4 * (i - 1)));
+            }
+          }
+          prev = acc;
+        });
+      }
+
+      // 4. d_W and d_bias over the four lanes' tiles of this chunk.
+      __syncthreads();
+      static_for<kHeadWaves>([&](auto QI) {
+        constexpr int q = decltype(QI)::value;
+        s16x4 bh[NT], bl[NT];
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          for (int rr = 0; rr < 4; ++rr) {
+            const int idx = (kL * q + 4 * g + rr) * S::GL_PITCH + 16 * ct + s;
+            bh[ct][rr] = static_cast<short>(s_ghi[idx]);
+            bl[ct][rr] = static_cast<short>(s_glo[idx]);
+          }
+        });
+        static_for<S::MW>([&](auto MI) {
+          constexpr int mi = decltype(MI)::value;
+          const int hb = w * Q + 16 * mi;
+          s16x4 ah;
+          for (int rr = 0; rr < 4; ++rr)
+            ah[rr] = static_cast<short>(s_h[(kL * q + 4 * g + rr) * S::HL_PITCH + hb + s]);
+          static_for<NT>([&](auto CT) {
+            constexpr int ct = decltype(CT)::value;
+            acc_w[mi][ct] = mfma_k16(ah, bh[ct], acc_w[mi][ct]);
+            acc_w[mi][ct] = mfma_k16(ah, bl[ct], acc_w[mi][ct]);
+          });
+        });
+        if (w == 0) {
+          const s16x4 ones = {0x3F80, 0x3F80, 0x3F80, 0x3F80};  // bfloat16 1.0
+          static_for<NT>([&](auto CT) {
+            constexpr int ct = decltype(CT)::value;
+            acc_b[ct] = mfma_k16(ones, bh[ct], acc_b[ct]);
+            acc_b[ct] = mfma_k16(ones, bl[ct], acc_b[ct]);
+          });
+        }
+      });
+      __syncthreads();
+    }
+
+    // This lane's loss sums (lanes of group 0 hold them), in a fixed order.
+#pragma unroll
+    for (int off = kL / 2; off > 0; off >>= 1) {
+      l_pg += __shfl_xor(l_pg, off, kL);
+      l_base += __shfl_xor(l_base, off, kL);
+      l_ent += __shfl_xor(l_ent, off, kL);
+    }
+    l_base *= a.baseline_cost;
+    l_ent *= a.entropy_cost;
+    if (l == 0 && lane_ok) {
+      if (a.lane_losses) {
+        a.lane_losses[3 * b + 0] = static_cast<float>(l_pg);
+        a.lane_losses[3 * b + 1] = static_cast<float>(l_base);
+        a.lane_losses[3 * b + 2] = static_cast<float>(l_ent);
+      }
+      wave_pg += l_pg;
+      wave_base += l_base;
+      wave_ent += l_ent;
+    }
+  }
+
+  // Partial sums of this workgroup: d_W rows [w H/4, (w+1) H/4), d_bias, losses.
+  float* part = a.grad_partials + static_cast<size_t>(blockIdx.x) * (H + 1) * C;
+  static_for<S::MW>([&](auto MI) {
+    constexpr int mi = decltype(MI)::value;
+    static_for<NT>([&](auto CT) {
+      constexpr int ct = decltype(CT)::value;
+      for (int jj = 0; jj < 4; ++jj)
+        part[(w * Q + 16 * mi + 4 * g + jj) * C + 16 * ct + s] = acc_w[mi][ct][jj];
+    });
+  });
+  if (w == 0 && g == 0) {
+    static_for<NT>([&](auto CT) {
+      constexpr int ct = decltype(CT)::value;
+      part[H * C + 16 * ct + s] = acc_b[ct][0];
+    });
+  }
+  if (l == 0) {
+    s_red[3 * w + 0] = wave_pg;
+    s_red[3 * w + 1] = wave_base;
+    s_red[3 * w + 2] = wave_ent;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double p0 = 0.0, p1 = 0.0, p2 = 0.0;
+    for (int i = 0; i < kHeadWaves; ++i) {
+      p0 += s_red[3 * i + 0];
+      p1 += s_red[3 * i + 1];
+      p2 += s_red[3 * i + 2];
+    }
+    double* lp = a.loss_partials + 3 * static_cast<size_t>(blockIdx.x);
+    lp[0] = p0;
+    lp[1] = p1;
+    lp[2] = p2;
+  }
+}
+
+// Adds the workgroups' partial sums in workgroup order (float64): d_W, d_bias
+// and the loss totals.  Block i covers 64 outputs; its four waves each sum a
+// quarter of the workgroups, and the quarters are added in order.
+constexpr int kFinishOutputs = 64;
+__global__ __launch_bounds__(256) void head_finish_kernel(HeadArgs a, int C, int nwg) {
+  __shared__ double s_q[4][kFinishOutputs];
+  const int64_t H = a.H;
+  const int A1 = static_cast<int>(a.A) + 1;
+  const int64_t n_w = H * A1;
+  const int64_t n_out = n_w + A1;
+  const int wv = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kFinishOutputs + lane;
+  const size_t stride = static_cast<size_t>(H + 1) * C;
+  size_t off = 0;
+  if (i < n_w)
+    off = static_cast<size_t>(i / A1) * C + static_cast<size_t>(i % A1);
+  else if (i < n_out)
+    off = static_cast<size_t>(H) * C + static_cast<size_t>(i - n_w);
+  const int per = (nwg + 3) / 4;
+  const int w0 = wv * per, w1 = (w0 + per < nwg) ? w0 + per : nwg;
+  double sum = 0.0;
+  if (i < n_out)
+    for (int k = w0; k < w1; ++k) sum += static_cast<double>(a.grad_partials[k * stride + off]);
+  s_q[wv][lane] = sum;
+  __syncthreads();
+  if (wv == 0 && i < n_out) {
+    const double tot = ((s_q[0][lane] + s_q[1][lane]) + s_q[2][lane]) + s_q[3][lane];
+    if (i < n_w)
+      a.d_weight[i] = static_cast<float>(tot);
+    else
+      a.d_bias[i - n_w] = static_cast<float>(tot);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    double p0 = 0.0, p1 = 0.0, p2 = 0.0;
+    for (int k = 0; k < nwg; ++k) {
+      p0 += a.loss_partials[3 * k + 0];
+      p1 += a.loss_partials[3 * k + 1];
+      p2 += a.loss_partials[3 * k + 2];
+    }
+    a.losses[0] = static_cast<float>(p0 + p1 + p2);
+    a.losses[1] = static_cast<float>(p0);
+    a.losses[2] = static_cast<float>(p1);
+    a.losses[3] = static_cast<float>(p2);
+  }
+}
+
+template <int H, int NT, typename BehIn>
+void launch_head_shape(const HeadArgs& a, hipStream_t st, unsigned nwg) {
+  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+  if (precise)
+    hipLaunchKernelGGL((head_kernel<H, NT, true, BehIn>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL((head_kernel<H, NT, false, BehIn>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
+}
+
+template <int H>
+void launch_head_h(const HeadArgs& a, hipStream_t st, unsigned nwg) {
+  const bool two = a.A + 1 > 16;
+  if (a.behaviour_bf16) {
+    if (two) launch_head_shape<H, 2, uint16_t>(a, st, nwg);
+    else launch_head_shape<H, 1, uint16_t>(a, st, nwg);
+  } else {
+    if (two) launch_head_shape<H, 2, float>(a, st, nwg);
+    else launch_head_shape<H, 1, float>(a, st, nwg);
+  }
+}
+
+int head_columns(int64_t A) { return A + 1 > 16 ? 32 : 16; }
+
+}  // namespace
+
+bool head_hidden_supported(int64_t H) { return H == 64 || H == 128 || H == 256; }
+
+int64_t head_workgroups(int64_t B) {
+  const int64_t quads = (B + kHeadWaves - 1) / kHeadWaves;
+  return quads < kHeadMaxWorkgroups ? quads : kHeadMaxWorkgroups;
+}
+
+namespace {
+size_t head_loss_bytes(int64_t B) {
+  const size_t n = 3 * sizeof(double) * static_cast<size_t>(head_workgroups(B));
+  return (n + 255) / 256 * 256;
+}
+}  // namespace
+
+size_t head_workspace_bytes(int64_t B, int64_t A, int64_t H) {
+  return kWsHeaderBytes + head_loss_bytes(B) +
+         sizeof(float) * static_cast<size_t>(head_workgroups(B)) * static_cast<size_t>(H + 1) *
+             static_cast<size_t>(head_columns(A));
+}
+
+void head_attach_workspace(HeadArgs* a, void* ws) {
+  char* base = static_cast<char*>(ws);
+  a->error_flag = reinterpret_cast<unsigned int*>(base + kWsFlagOffset);
+  a->loss_partials = reinterpret_cast<double*>(base + kWsHeaderBytes);
+  a->grad_partials = reinterpret_cast<float*>(base + kWsHeaderBytes + head_loss_bytes(a->B));
+}
+
+hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
+  const int64_t nwg = head_workgroups(a.B);
+  const unsigned n = static_cast<unsigned>(nwg);
+  if (a.H == 64) launch_head_h<64>(a, st, n);
+  else if (a.H == 128) launch_head_h<128>(a, st, n);
+  else if (a.H == 256) launch_head_h<256>(a, st, n);
+  else return hipErrorInvalidValue;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t n_out = a.H * (a.A + 1) + (a.A + 1);
+  const unsigned fb = static_cast<unsigned>((n_out + kFinishOutputs - 1) / kFinishOutputs);
+  hipLaunchKernelGGL(head_finish_kernel, dim3(fb), dim3(256), 0, st, a, head_columns(a.A),
+                     static_cast<int>(nwg));
+  return hipGetLastError();
+}
+
+}  // namespace vtrace

@@ -1,0 +1,85 @@
+// Wave-level helpers shared by the tiled kernels (gfx950, wave64): compile-time
+// loops, DPP row moves, exponentials and the XCD-aware workgroup numbering.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <utility>
+
+namespace vtrace {
+
+// A native 16-byte vector: plain vector loads and stores, kept in registers.
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+// Calls f(std::integral_constant<int, i>) for i = 0..N-1, unrolled at compile
+// time so that arrays indexed by i stay in registers.
+template <typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// DPP row moves on a double (two 32-bit halves).  Lanes whose source falls
+// outside their row of 16 keep their own value.
+//   0x100 + k (row_shl:k): lane i of a row reads lane i+k;
+//   kRowShr15 (row_shr:15): lane 15 of a row reads lane 0.
+template <int kCtrl>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const unsigned long long u = __double_as_longlong(x);
+  int lo = static_cast<int>(u & 0xffffffffu);
+  int hi = static_cast<int>(u >> 32);
+  lo = __builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
+  hi = __builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
+  return __longlong_as_double(static_cast<long long>(
+      (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+constexpr int kRowShl1 = 0x101;
+constexpr int kRowShr15 = 0x11F;
+
+// e^x from the hardware base-2 exponential (about one ulp; results below the
+// normal range flush to zero, harmless where every term joins a sum >= 1).
+__device__ __forceinline__ float exp_fast(float x) {
+  constexpr float kLog2e = 1.44269504088896340736f;
+  return __builtin_amdgcn_exp2f(x * kLog2e);
+}
+
+// e^x in float64 for finite x <= 0: Cody-Waite reduction x = k ln2 + r with
+// |r| <= ln2/2 (ln2 split into a 32-bit head, so k*head is exact, and a tail),
+// then the Taylor series of e^r to degree 9 (truncation below 7e-12 relative)
+// and a scaling by 2^k.  Arguments below -1000 are raised to -1000, where the
+// result has already underflowed to zero; NaN stays NaN.
+__device__ __forceinline__ double exp_nonpos_f64(double x) {
+  constexpr double kLog2e = 1.4426950408889634;
+  constexpr double kLn2Hi = 0.6931471803691238;      // ln2 rounded to 32 bits
+  constexpr double kLn2Lo = 1.9082149292705877e-10;  // ln2 - kLn2Hi
+  x = x < -1000.0 ? -1000.0 : x;
+  const double k = __builtin_rint(x * kLog2e);
+  double r = fma(-k, kLn2Hi, x);
+  r = fma(-k, kLn2Lo, r);
+  double p = 2.7557319223985893e-06;  // 1/9!
+  p = fma(p, r, 2.48015873015873e-05);
+  p = fma(p, r, 0.0001984126984126984);
+  p = fma(p, r, 0.001388888888888889);
+  p = fma(p, r, 0.008333333333333333);
+  p = fma(p, r, 0.041666666666666664);
+  p = fma(p, r, 0.16666666666666666);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  return __builtin_ldexp(p, static_cast<int>(k));
+}
+
+// Workgroups are handed to the 8 XCDs round-robin; number the lane tiles so
+// that neighbouring tiles (which share 128-byte lines of the [T,B] arrays) run
+// on the same XCD and meet in its L2.
+__device__ __forceinline__ int64_t xcd_tile(int64_t block, int64_t nblocks) {
+  constexpr int64_t kXcd = 8;
+  const int64_t per = nblocks / kXcd;
+  if (block >= per * kXcd) return block;
+  return (block % kXcd) * per + block / kXcd;
+}
+
+}  // namespace vtrace

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 13
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(_lib.SIGNATURES)
@@ -205,3 +205,55 @@ def test_python_binding_validates_before_calling():
                          torch.zeros(2, 3), torch.zeros(2, 3), torch.zeros(3))
     with pytest.raises(TypeError):
         v.binding._dtype_code(torch.zeros(1, dtype=torch.float16))
+
+
+def _head(L, **kw):
+    V = _lib.Variant
+    a = dict(T=5, B=4, A=9, H=64, dt=0, h=P, W=P, bias=P, beh=P, act=P, r=P, d=P, boot=P, rho=1.0,
+             c=1.0, lam=1.0, cv=0.5, ce=0.01, variant=None, losses=P, dh=P, dW=P, db=P, vs=None,
+             pg=None, lane=None, outs=None, ws=P, nws=1 << 24)
+    a.update(kw)
+    return L.vtrace_head_loss_grad(a["T"], a["B"], a["A"], a["H"], a["dt"], a["h"], a["W"], a["bias"],
+                                   a["beh"], a["act"], a["r"], a["d"], a["boot"], a["rho"], a["c"],
+                                   a["lam"], a["cv"], a["ce"], a["variant"], a["losses"], a["dh"],
+                                   a["dW"], a["db"], a["vs"], a["pg"], a["lane"], a["outs"], a["ws"],
+                                   a["nws"], None)
+
+
+def test_head_workspace_bytes(L):
+    n = L.vtrace_head_workspace_bytes
+    assert n(5, 4, 9, 64) >= 256 + 3 * 8 + 65 * 16 * 4
+    assert n(5, 4, 16, 64) > n(5, 4, 15, 64)  # 17 outputs need two column tiles
+    assert n(1000, 16384, 18, 256) == n(1, 16384, 18, 256)
+    for bad in ((0, 4, 9, 64), (5, 0, 9, 64), (5, 4, 0, 64), (5, 4, 32, 64), (5, 4, 9, 100),
+                (5, 4, 9, 512), (1 << 21, 1 << 20, 9, 64)):
+        assert n(*bad) == 0, bad
+
+
+HEAD_INVALID = [
+    (dict(h=None), NULL), (dict(W=None), NULL), (dict(bias=None), NULL), (dict(beh=None), NULL),
+    (dict(act=None), NULL), (dict(r=None), NULL), (dict(d=None), NULL), (dict(boot=None), NULL),
+    (dict(losses=None), NULL), (dict(dh=None), NULL), (dict(dW=None), NULL), (dict(db=None), NULL),
+    (dict(T=0), SHAPE), (dict(A=32), SHAPE), (dict(A=0), SHAPE), (dict(H=96), SHAPE),
+    (dict(H=512), SHAPE), (dict(dt=5), DTYPE),
+    (dict(rho=math.nan), PARAM), (dict(lam=1.5), PARAM), (dict(cv=math.inf), PARAM),
+    (dict(h=P + 8), ALIGN), (dict(dh=P + 8), ALIGN), (dict(W=P + 1), ALIGN), (dict(beh=P + 2), ALIGN),
+    (dict(bias=P + 2), ALIGN), (dict(outs=P + 2), ALIGN),
+    (dict(ws=None), WS), (dict(nws=1024), WS), (dict(ws=P + 8), ALIGN),
+]
+
+
+@pytest.mark.parametrize("kw,status", HEAD_INVALID)
+def test_head_rejects(L, kw, status):
+    assert _head(L, **kw) == status
+
+
+def test_head_variant_and_behaviour_alignment(L):
+    V = _lib.Variant
+    assert _head(L, variant=ctypes.byref(V(5, 0, 0.0))) == PARAM
+    assert _head(L, variant=ctypes.byref(V(0, 0, 0.0, 0, 0, 3))) == DTYPE
+    # bfloat16 behaviour logits are read element by element: 2-byte alignment,
+    # checked together with another invalid argument so that nothing launches
+    assert _head(L, dt=1, beh=P + 2, T=0) == SHAPE
+    assert _head(L, dt=1, beh=P + 1) == ALIGN
+    assert _head(L, variant=ctypes.byref(V(0, 0, 0.0, 1, 0, 0)), beh=P + 2) == ALIGN
