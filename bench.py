@@ -10,6 +10,10 @@ holds K back-to-back calls.  Prints one JSON line on stdout.
 Default workload: the stress batch, T=1000, B=16384, A=18, fp32 logits,
 rho_bar = c_bar = lambda = 1 (3.87 GB of algorithmic traffic per step, far
 beyond the 256 MB Infinity Cache, so no cache flush is needed between steps).
+
+``--head`` times vtrace_head_loss_grad instead: the learner's output layer
+(hidden size 256, bfloat16) fused with the same V-trace step and the gradients
+through the layer, on the stress shape drawn on the device.
 """
 
 from __future__ import annotations
@@ -29,6 +33,10 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, AMD's published peak
 METRIC = "trajectory steps/sec (T*B) for fused V-trace loss+grad; achieved HBM GB/s"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "loss_grad_stress_counters.json")
+HEAD_COUNTERS_FILE = os.path.join(ROOT, "profiles", "head_stress_counters.json")
+# The sources each counted kernel is built from.
+PLAIN_SOURCES = ("tiled.hip", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
+HEAD_SOURCES = ("head.hip", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
 
 
 def parse_args():
@@ -49,6 +57,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
+    ap.add_argument("--head", action="store_true",
+                    help="time the fused output layer + V-trace call (stress shape, H=256)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run plain device-to-device copies of MIB MiB (the reference "
                          "kernel for scaling HBM byte counters), then exit")
@@ -95,15 +105,15 @@ def calibrate_copy(mib, reps):
                       "add_2read_1write_GBps": 3 * n * 4 / mix_ms / 1e6}), flush=True)
 
 
-def kernel_source_digest() -> str:
-    """Hash of the HIP sources, to tell whether stored counters still describe them."""
+def kernel_source_digest(files=PLAIN_SOURCES) -> str:
+    """Hash of the HIP sources a kernel is built from, to tell whether stored
+    counters still describe it."""
     csrc = os.path.join(ROOT, "paper_1802_01561_amd", "csrc")
     h = hashlib.sha256()
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".hpp")):
-            h.update(f.encode())
-            with open(os.path.join(csrc, f), "rb") as fh:
-                h.update(fh.read())
+    for f in sorted(files):
+        h.update(f.encode())
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -130,17 +140,17 @@ def to_device(tr, torch, np):
                 bootstrap_value=d(tr.bootstrap_value))
 
 
-def stored_traffic(avg_kernel_ms):
+def stored_traffic(avg_kernel_ms, path=COUNTERS_FILE, files=PLAIN_SOURCES):
     """Counted HBM traffic of one launch, from committed rocprofv3 FETCH_SIZE and
     WRITE_SIZE runs scaled by the same counters' readings for a plain copy of
     known size, as (GB/s over this run's average launch time, bytes per launch).
     None when the counters are missing or were taken on other kernel sources."""
     try:
-        with open(COUNTERS_FILE) as fh:
+        with open(path) as fh:
             c = json.load(fh)
     except (OSError, ValueError):
         return None, None
-    if c.get("kernel_source_digest") != kernel_source_digest():
+    if c.get("kernel_source_digest") != kernel_source_digest(files):
         return None, None
     nbytes = c["hbm_bytes_per_launch"]
     return nbytes / (avg_kernel_ms * 1e-3) / 1e9, nbytes
@@ -174,15 +184,6 @@ def cpu_baseline(tr, p, target_s):
         t = run(n)
     n = int(min(tr.B, max(n, n * target_s / max(t, 1e-6))))
     wall = run(n)
-    cpu_model = platform.processor()
-    try:
-        with open("/proc/cpuinfo") as fh:
-            for line in fh:
-                if line.startswith("model name"):
-                    cpu_model = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
     return {
         "value": tr.T * n / wall,
         "unit": "steps/s",
@@ -190,9 +191,174 @@ def cpu_baseline(tr, p, target_s):
         "kind": "oracle",
         "sample": f"{n} of {tr.B} lanes x all T={tr.T} steps ({tr.T * n} steps) of the same "
                   f"batch, fp64 NumPy oracle, one thread, {wall:.1f} s wall",
-        "cpu_model": cpu_model,
+        "cpu_model": cpu_model(),
         "host_cpus": os.cpu_count(),
     }
+
+
+def cpu_model():
+    name = platform.processor()
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return name
+
+
+def timed_calls(step, K, W, stream):
+    """W untimed calls, then K calls bracketed by synchronisations, each between
+    two HIP events on the launch stream.  Returns (per-call event ms, wall ms
+    per call)."""
+    import numpy as np
+    import torch
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]), (t1 - t0) * 1e3 / K
+
+
+def head_algorithmic_bytes(T, B, A, H, grad_bytes):
+    """Bytes the fused output-layer call must move: per step the hidden row
+    (bfloat16), the behaviour logit row, action, reward and discount in and the
+    d_hidden row out; per call the bootstrap values, the layer's parameters in
+    and their gradients out."""
+    per_step = 2 * H + 4 * A + 12 + grad_bytes * H
+    per_call = 4 * B + (2 * H * (A + 1) + 4 * (A + 1)) + (4 * H * (A + 1) + 4 * (A + 1) + 16)
+    return T * B * per_step + per_call, per_step
+
+
+def head_cpu_baseline(d, p, target_s, T, B):
+    """The fp64 oracle of the fused call, as it stands, on a bounded sample of
+    lanes (all T) copied back from the device, one host thread."""
+    import numpy as np
+    import oracle
+    from synth import head_batch_from_device
+
+    def run(n):
+        wall = 0.0
+        for l0 in range(0, n, 256):
+            hb = head_batch_from_device(d, list(range(l0, min(n, l0 + 256))))
+            t0 = time.perf_counter()
+            oracle.head_loss_and_grads(hb.hidden, hb.weight, hb.bias, hb.behaviour_logits,
+                                       hb.actions, hb.rewards, hb.discounts, hb.bootstrap_value,
+                                       p.rho_bar, p.c_bar, p.lam, p.baseline_cost, p.entropy_cost)
+            wall += time.perf_counter() - t0
+        return wall
+
+    n = 16
+    t = run(n)
+    while t < target_s / 16 and n < B:
+        n = min(B, n * 4)
+        t = run(n)
+    n = int(min(B, max(n, n * target_s / max(t, 1e-6))))
+    wall = run(n)
+    return {
+        "value": T * n / wall,
+        "unit": "steps/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{n} of {B} lanes x all T={T} steps ({T * n} steps) of the same batch, "
+                  f"fp64 NumPy oracle of the output layer + V-trace, {wall:.1f} s wall",
+        "cpu_model": cpu_model(),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def run_head(args):
+    """The fused output layer + V-trace call on the stress shape with H = 256."""
+    import numpy as np
+    import torch
+
+    import paper_1802_01561_amd as vt
+    from synth import HEAD_CONFIGS, SEED_BASE, Params, make_head_device
+
+    c = HEAD_CONFIGS["stress"]
+    T, B, A, H = c["T"], c["B"], c["A"], c["H"]
+    seed = SEED_BASE + 1004
+    p = Params()
+    t_gen = time.perf_counter()
+    d = make_head_device(T, B, A, H, seed, "cuda")
+    torch.cuda.synchronize()
+    print(f"[bench] head stress T={T} B={B} A={A} H={H} {p.label()} "
+          f"(generated on the device in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr,
+          flush=True)
+    grad_dtype = torch.bfloat16 if args.grad_bf16 else torch.float32
+    ws = vt.Workspace(T, B, A, H=H)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    out = vt.HeadLossGrad(torch.empty(4, **f32), torch.empty((T, B, H), dtype=grad_dtype, device="cuda"),
+                          torch.empty((H, A + 1), **f32), torch.empty(A + 1, **f32),
+                          None, None, None, None)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        vt.vtrace_head_loss_grad(d["hidden"], d["weight"], d["bias"], d["behaviour_logits"],
+                                 d["actions"], d["rewards"], d["discounts"], d["bootstrap_value"],
+                                 p.rho_bar, p.c_bar, p.lam, p.baseline_cost, p.entropy_cost,
+                                 workspace=ws, out=out, grad_dtype=grad_dtype)
+
+    call_ms, ms_per_step = timed_calls(step, args.steps, args.warmup, stream)
+    avg_ms = float(call_ms.mean())
+    grad_bytes = 2 if args.grad_bf16 else 4
+    alg_bytes, per_step = head_algorithmic_bytes(T, B, A, H, grad_bytes)
+    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    mfma_flop = 3 * 2 * T * B * H * (A + 1)  # forward, d_hidden, d_weight
+    print(f"[bench] head call avg {avg_ms:.4f} ms (min {call_ms.min():.4f}); wall "
+          f"{ms_per_step:.4f} ms/step; {achieved:.1f} GB/s algorithmic; "
+          f"{mfma_flop / (avg_ms * 1e-3) / 1e12:.1f} TFLOP/s of matrix products; losses "
+          f"{out.losses.cpu().tolist()}", file=sys.stderr, flush=True)
+    counted = not args.grad_bf16
+    traffic, traffic_bytes = (stored_traffic(avg_ms, HEAD_COUNTERS_FILE, HEAD_SOURCES) if counted
+                              else (None, None))
+    result = {
+        "metric": METRIC,
+        "value": T * B / (ms_per_step * 1e-3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16-mfma/f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"stress + output layer: T={T} B={B} A={A} H={H}, bf16 hidden and "
+                        f"weights, f32 behaviour logits, {'bf16' if args.grad_bf16 else 'f32'} "
+                        f"d_hidden, rho_bar=c_bar=lambda=1",
+            "T": T, "B": B, "A": A, "H": H, "seed": seed,
+        },
+        "kernel_ms_avg": avg_ms,
+        "kernel_ms_min": float(call_ms.min()),
+        "alg_bytes_per_launch": alg_bytes,
+        "alg_bytes_per_step": per_step,
+        "traffic_bytes_per_launch": traffic_bytes,
+        "mfma_tflops": mfma_flop / (avg_ms * 1e-3) / 1e12,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = head_cpu_baseline(d, p, args.cpu_seconds, T, B)
+    print(json.dumps(result), flush=True)
 
 
 def main():
@@ -207,6 +373,14 @@ def main():
         return
     if args.kernel == "lane_serial":
         os.environ["VTRACE_KERNEL"] = "lane_serial"
+    if args.head:
+        import torch
+        if not torch.cuda.is_available():
+            print("bench.py needs a GPU", file=sys.stderr)
+            sys.exit(1)
+        torch.cuda.set_device(0)
+        run_head(args)
+        return
 
     import numpy as np
     import torch
@@ -247,24 +421,8 @@ def main():
                             workspace=ws, out=out, correction=args.correction, behaviour=behaviour,
                             reward_transform=args.reward_transform, grad_dtype=grad_dtype)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
     K = args.steps
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        starts[i].record(stream)
-        step()
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-
-    kernel_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    ms_per_step = (t1 - t0) * 1e3 / K
+    kernel_ms, ms_per_step = timed_calls(step, K, args.warmup, stream)
     steps_per_s = T * B / (ms_per_step * 1e-3)
     logit_bytes = 2 if args.bf16 else 4
     alg_bytes, per_step = algorithmic_bytes(T, B, A, logit_bytes, args.log_probs,

@@ -214,6 +214,7 @@ class LossGradOut(NamedTuple):
     d_values: np.ndarray  # [T, B]
     vs: np.ndarray
     pg_advantages: np.ndarray
+    step_losses: np.ndarray  # [T, B, 3]: the per-step terms the lane losses sum
 
 
 def _pg_log_prob(log_pi_a, correction, epsilon):
@@ -277,4 +278,5 @@ def loss_and_grads(target_logits, behaviour_logits, actions, rewards, discounts,
     d_logits = ((vt.pg_advantages * w)[..., None] * (pi - onehot)
                 + c_e * pi * (log_pi + entropy[..., None]))
     d_values = c_v * (_f64(values) - vt.vs)
-    return LossGradOut(losses, lane, d_logits, d_values, vt.vs, vt.pg_advantages)
+    step_losses = np.stack([pg_tb, base_tb, ent_tb], axis=-1)
+    return LossGradOut(losses, lane, d_logits, d_values, vt.vs, vt.pg_advantages, step_losses)

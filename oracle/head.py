@@ -42,6 +42,7 @@ class HeadOut(NamedTuple):
     d_outputs: np.ndarray    # [T, B, A + 1]: G = [d_logits, d_values]
     vs: np.ndarray           # [T, B]
     pg_advantages: np.ndarray
+    step_losses: np.ndarray  # [T, B, 3]: per-step policy-gradient, baseline, entropy terms
 
 
 def head_forward(hidden, weight, bias):
@@ -69,7 +70,7 @@ def head_loss_and_grads(hidden, weight, bias, behaviour_logits, actions, rewards
     d_weight = hidden.reshape(-1, H).T @ G.reshape(-1, A + 1)
     d_bias = G.reshape(-1, A + 1).sum(axis=0)
     return HeadOut(lg.losses, lg.lane_losses, d_hidden, d_weight, d_bias, o, G, lg.vs,
-                   lg.pg_advantages)
+                   lg.pg_advantages, lg.step_losses)
 
 
 def sum_term_scale(hidden, d_outputs):

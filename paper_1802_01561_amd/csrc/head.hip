@@ -16,9 +16,11 @@
 // chunk the 16 steps of the wave's lane are the 16 rows of one MFMA tile; lane
 // l of the wave is (s, g) = (l % 16, l / 16).
 //  1. Forward, o^T = W^T hidden^T with 16x16x32 MFMAs (M: output column, N:
-//     step, K: hidden unit).  Lane (s, g) loads the K slice [g H/4, (g+1) H/4)
-//     of step s's hidden row as whole 16-byte vectors and receives o[s][4g + i]
-//     (and o[s][16 + 4g + i] when A + 1 > 16), i = 0..3.
+//     step, K: hidden unit).  In K step j, lane (s, g) supplies hidden units
+//     32j + 8g .. 32j + 8g + 7 of step s's row, one 16-byte vector: the four
+//     lane groups read 64 contiguous bytes of each row per instruction and the
+//     next K step the rest of the 128-byte line.  The lane receives
+//     o[s][4g + i] (and o[s][16 + 4g + i] when A + 1 > 16), i = 0..3.
 //  2. The V-trace epilogue works in that layout.  Row statistics of a step
 //     (maxima, exponent sums, the taken action's logit, the baseline) are sums
 //     over the four lane groups: two xor shuffles, whose fixed order gives all
@@ -30,8 +32,9 @@
 //     contraction order, so G enters the MFMA where the epilogue left it.  G
 //     is split into bfloat16 high and low parts (hi + lo equals G to within
 //     2^-17 relative), two MFMAs, so the product keeps float32 accuracy.  The
-//     M rows (hidden units) are ordered so that each lane receives H/4
-//     consecutive units of its step's row: whole 16-byte stores.
+//     M rows (hidden units) are ordered so that M tiles 2p and 2p+1 give lane
+//     (s, g) units 32p + 8g .. 32p + 8g + 7 of its step's row: the four lane
+//     groups store 64 (bfloat16) or 2 x 64 (float32) contiguous bytes per row.
 //  4. d_W contracts over steps, which lie across lanes: the hidden tile and G
 //     are written to LDS, and after a workgroup barrier wave w accumulates
 //     rows [w H/4, (w+1) H/4) of d_W over the four lanes' tiles with 16x16x16
@@ -56,7 +59,7 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 template <int H, int NT>
 struct HeadShape {
   static constexpr int C = 16 * NT;     // output columns covered by the MFMA tiles
-  static constexpr int Q = H / 4;       // hidden units per lane group
+  static constexpr int Q = H / 4;       // hidden units each wave's d_W tiles cover
   static constexpr int KS = H / 32;     // forward K steps = 16-byte vectors per lane and row
   static constexpr int MT = H / 16;     // d_hidden M tiles
   static constexpr int MW = H / 64;     // d_W M tiles per wave
@@ -183,10 +186,10 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
       int64_t t = T - static_cast<int64_t>(k + 1) * kL + s;
       t = t < 0 ? 0 : t;  // rows before t = 0 reread row 0 and are masked later
       const int64_t row = t * B + (lane_ok ? b : 0);
-      const v4u* hp = reinterpret_cast<const v4u*>(a.hidden + row * H + g * Q);
+      const uint16_t* hp = a.hidden + row * H + 8 * g;
       static_for<S::KS>([&](auto J) {
         constexpr int j = decltype(J)::value;
-        hreg[j] = lane_ok ? __builtin_nontemporal_load(hp + j) : v4u{0u, 0u, 0u, 0u};
+        hreg[j] = lane_ok ? *reinterpret_cast<const v4u*>(hp + 32 * j) : v4u{0u, 0u, 0u, 0u};
       });
       if (lane_ok) {
         p_act = a.actions[row];
@@ -219,18 +222,18 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         static_for<NT>([&](auto CT) {
           constexpr int ct = decltype(CT)::value;
           const bf16x8 wv =
-              *reinterpret_cast<const bf16x8*>(&s_wt[(16 * ct + s) * S::WT_PITCH + g * Q + 8 * j]);
+              *reinterpret_cast<const bf16x8*>(&s_wt[(16 * ct + s) * S::WT_PITCH + 32 * j + 8 * g]);
           oacc[ct] = mfma_k32(wv, hv, oacc[ct]);
         });
       });
       // The hidden slice goes to LDS for d_W (the previous chunk's readers
       // finished at its closing barrier).
       {
-        uint16_t* hrow = s_h + (kL * w + s) * S::HL_PITCH + g * Q;
+        uint16_t* hrow = s_h + (kL * w + s) * S::HL_PITCH + 8 * g;
         static_for<S::KS>([&](auto J) {
           constexpr int j = decltype(J)::value;
-          reinterpret_cast<uint2*>(hrow + 8 * j)[0] = uint2{hreg[j].x, hreg[j].y};
-          reinterpret_cast<uint2*>(hrow + 8 * j)[1] = uint2{hreg[j].z, hreg[j].w};
+          reinterpret_cast<uint2*>(hrow + 32 * j)[0] = uint2{hreg[j].x, hreg[j].y};
+          reinterpret_cast<uint2*>(hrow + 32 * j)[1] = uint2{hreg[j].z, hreg[j].w};
         });
       }
       int32_t act = p_act;
@@ -439,19 +442,18 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = (s / 4) * Q + 4 * i + (s % 4);
+          const int hrow = 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4);
           const bf16x8 wv = *reinterpret_cast<const bf16x8*>(&s_wp[hrow * S::WP_PITCH + 8 * g]);
           f32x4 acc = mfma_k32(wv, ghi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k32(wv, glo, acc);
           if (step_ok) {
+            const int64_t hcol = 32 * (i / 2) + 8 * g;
             if (!grad_bf16) {
-              __builtin_nontemporal_store(
-                  acc, reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + g * Q + 4 * i));
+              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + hcol + 4 * (i % 2)) = acc;
             } else if (i % 2 == 1) {
               const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
                               pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
-              __builtin_nontemporal_store(
-                  pk, reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + g * Q + 4 * (i - 1)));
+              *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
             }
           }
           prev = acc;
@@ -466,19 +468,18 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = (s / 4) * Q + 4 * i + (s % 4);
+          const int hrow = 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4);
           const s16x4 wv = *reinterpret_cast<const s16x4*>(&s_wp[hrow * S::WP_PITCH + 4 * g]);
           f32x4 acc = mfma_k16(wv, shi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k16(wv, slo, acc);
           if (step_ok) {
+            const int64_t hcol = 32 * (i / 2) + 8 * g;
             if (!grad_bf16) {
-              __builtin_nontemporal_store(
-                  acc, reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + g * Q + 4 * i));
+              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + hcol + 4 * (i % 2)) = acc;
             } else if (i % 2 == 1) {
               const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
                               pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
-              __builtin_nontemporal_store(
-                  pk, reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + g * Q + 4 * (i - 1)));
+              *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
             }
           }
           prev = acc;

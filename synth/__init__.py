@@ -8,6 +8,7 @@ the HIP path consume what it produces, and neither imports the other.
 from .trajectories import (  # noqa: F401
     CONFIGS,
     PARAM_SETS,
+    SEED_BASE,
     Params,
     Trajectories,
     bf16_bits_to_f32,
