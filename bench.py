@@ -36,7 +36,7 @@ COUNTERS_FILE = os.path.join(ROOT, "profiles", "loss_grad_stress_counters.json")
 HEAD_COUNTERS_FILE = os.path.join(ROOT, "profiles", "head_stress_counters.json")
 # The sources each counted kernel is built from.
 PLAIN_SOURCES = ("tiled.hip", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
-HEAD_SOURCES = ("head.hip", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
+HEAD_SOURCES = ("head.hip", "head.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
 
 
 def parse_args():

@@ -5,6 +5,7 @@
 #include <cstring>
 
 #include "../../include/vtrace.h"
+#include "head.hpp"
 #include "launch.hpp"
 
 namespace {

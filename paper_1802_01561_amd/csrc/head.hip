@@ -32,15 +32,17 @@
 //     contraction order, so G enters the MFMA where the epilogue left it.  G
 //     is split into bfloat16 high and low parts (hi + lo equals G to within
 //     2^-17 relative), two MFMAs, so the product keeps float32 accuracy.  The
-//     M rows (hidden units) are ordered so that M tiles 2p and 2p+1 give lane
-//     (s, g) units 32p + 8g .. 32p + 8g + 7 of its step's row: the four lane
-//     groups store 64 (bfloat16) or 2 x 64 (float32) contiguous bytes per row.
+//     M rows (hidden units) are ordered for whole 64-byte runs per row and
+//     store instruction: M tile i gives lane (s, g) units 16i + 4g .. +3 of
+//     its step's row for float32 output, and M tiles 2p and 2p+1 give it units
+//     32p + 8g .. +7 (one 16-byte vector) for bfloat16 output.
 //  4. d_W contracts over steps, which lie across lanes: the hidden tile and G
 //     are written to LDS, and after a workgroup barrier wave w accumulates
 //     rows [w H/4, (w+1) H/4) of d_W over the four lanes' tiles with 16x16x16
 //     MFMAs, in registers, for the whole walk (wave 0 also d_bias, with a ones
 //     operand).  A second kernel adds the workgroups' partial sums.
 #include "device_common.hpp"
+#include "head.hpp"
 #include "wave_ops.hpp"
 
 namespace vtrace {
@@ -442,15 +444,15 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4);
+          const int hrow = grad_bf16 ? 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4) : 16 * i + s;
           const bf16x8 wv = *reinterpret_cast<const bf16x8*>(&s_wp[hrow * S::WP_PITCH + 8 * g]);
           f32x4 acc = mfma_k32(wv, ghi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k32(wv, glo, acc);
           if (step_ok) {
-            const int64_t hcol = 32 * (i / 2) + 8 * g;
             if (!grad_bf16) {
-              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + hcol + 4 * (i % 2)) = acc;
+              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + 16 * i + 4 * g) = acc;
             } else if (i % 2 == 1) {
+              const int64_t hcol = 32 * (i / 2) + 8 * g;
               const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
                               pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
               *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
@@ -468,15 +470,15 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4);
+          const int hrow = grad_bf16 ? 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4) : 16 * i + s;
           const s16x4 wv = *reinterpret_cast<const s16x4*>(&s_wp[hrow * S::WP_PITCH + 4 * g]);
           f32x4 acc = mfma_k16(wv, shi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k16(wv, slo, acc);
           if (step_ok) {
-            const int64_t hcol = 32 * (i / 2) + 8 * g;
             if (!grad_bf16) {
-              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + hcol + 4 * (i % 2)) = acc;
+              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + 16 * i + 4 * g) = acc;
             } else if (i % 2 == 1) {
+              const int64_t hcol = 32 * (i / 2) + 8 * g;
               const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
                               pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
               *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
