@@ -147,7 +147,7 @@ vtrace_status apply_variant(const vtrace_variant* v, StepArgs* a) {
 
 bool head_shape_ok(int64_t T, int64_t B, int64_t A, int64_t H) {
   return A >= 1 && A <= vtrace::kHeadMaxActions && vtrace::head_hidden_supported(H) &&
-         shape_ok(T, B, H) &&
+         B <= vtrace::kHeadMaxBatchTimesHidden / H && shape_ok(T, B, H) &&
          shape_ok(T, B, A + 1);
 }
 

@@ -32,15 +32,17 @@
 //     contraction order, so G enters the MFMA where the epilogue left it.  G
 //     is split into bfloat16 high and low parts (hi + lo equals G to within
 //     2^-17 relative), two MFMAs, so the product keeps float32 accuracy.  The
-//     M rows (hidden units) are ordered for whole 64-byte runs per row and
-//     store instruction: M tile i gives lane (s, g) units 16i + 4g .. +3 of
-//     its step's row for float32 output, and M tiles 2p and 2p+1 give it units
-//     32p + 8g .. +7 (one 16-byte vector) for bfloat16 output.
+//     M rows (hidden units) are ordered so that each store instruction of the
+//     four lane groups writes 64 contiguous bytes of a row: for float32 output
+//     M tile i gives lane (s, g) units 16i + 4g .. +3, for bfloat16 output M
+//     tiles 2p and 2p+1 give it units 32p + 8g .. +7 (one packed vector).
 //  4. d_W contracts over steps, which lie across lanes: the hidden tile and G
 //     are written to LDS, and after a workgroup barrier wave w accumulates
 //     rows [w H/4, (w+1) H/4) of d_W over the four lanes' tiles with 16x16x16
 //     MFMAs, in registers, for the whole walk (wave 0 also d_bias, with a ones
 //     operand).  A second kernel adds the workgroups' partial sums.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "head.hpp"
 #include "wave_ops.hpp"
@@ -57,6 +59,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
 template <int H, int NT>
 struct HeadShape {
@@ -111,12 +114,38 @@ __device__ __forceinline__ f32x4 mfma_k16(s16x4 a, s16x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
 
+// Global memory inside the chunk walk goes through raw buffer descriptors.
+// A load at an offset beyond the descriptor's size returns zero and a store
+// there is dropped, so rows before t = 0, lanes beyond B and outputs the caller
+// did not ask for are masked by their offsets or an empty descriptor, with no
+// branch around any memory instruction.  That keeps the count of outstanding
+// memory operations the same on every path, so the compiler can wait for the
+// prefetched loads alone (vmcnt(n)) rather than for every store before them.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRawBufferFlags = 0x00020000;  // raw buffer, 32-bit elements, no swizzle
+constexpr uint32_t kOutOfRange = 0xFFFFF000u;  // beyond every descriptor used here
+// s_waitcnt immediate for vmcnt(0) alone (expcnt and lgkmcnt at their maxima).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
+                                           kRawBufferFlags);
+}
+__device__ __forceinline__ float buffer_load_f32(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
 template <typename BehIn>
-__device__ __forceinline__ float load_behaviour(const void* p, int64_t i) {
-  return logit_to_float(static_cast<const BehIn*>(p)[i]);
+__device__ __forceinline__ float buffer_load_logit(Rsrc r, uint32_t off) {
+  if constexpr (sizeof(BehIn) == 4)
+    return buffer_load_f32(r, off);
+  else
+    return logit_to_float(static_cast<uint16_t>(__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0)));
+}
+__device__ __forceinline__ void buffer_store_f32(float x, Rsrc r, uint32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, off, 0, 0);
 }
 
-template <int H, int NT, bool kPrecise, typename BehIn>
+template <int H, int NT, bool kPrecise, typename BehIn, bool kBf16Grad>
 __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
   using S = HeadShape<H, NT>;
   constexpr int C = S::C, Q = S::Q;
@@ -126,9 +155,13 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
   __shared__ __align__(16) uint16_t s_ghi[kHeadWaves * kL * S::GL_PITCH];
   __shared__ __align__(16) uint16_t s_glo[kHeadWaves * kL * S::GL_PITCH];
   __shared__ double s_red[3 * kHeadWaves];
+  __shared__ float s_bias[C];
+  __shared__ float s_db[C];  // wave 0's running d_bias
 
   const int tid = threadIdx.x;
-  const int w = tid / kWave;
+  // The wave index, stated as wave-uniform so that lane numbers and buffer
+  // descriptors derived from it live in scalar registers.
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int l = tid % kWave;
   const int s = l % kL;  // step within the chunk (and row of MFMA operands)
   const int g = l / kL;  // lane group
@@ -143,30 +176,41 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
     s_wt[c * S::WT_PITCH + h] = v;
     s_wp[h * S::WP_PITCH + slot_of_column<NT>(c)] = v;
   }
-  float bias[NT][4];
-  static_for<NT>([&](auto CT) {
-    constexpr int ct = decltype(CT)::value;
-    for (int i = 0; i < 4; ++i) {
-      const int c = 16 * ct + 4 * g + i;
-      bias[ct][i] = c < A1 ? a.bias[c] : 0.0f;
-    }
-  });
+  if (tid < C) {
+    s_bias[tid] = tid < A1 ? a.bias[tid] : 0.0f;
+    s_db[tid] = 0.0f;
+  }
   __syncthreads();
 
   const bool beh_lp = a.behaviour_log_probs != 0;
   const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
   const bool use_y = !beh_lp && !no_ratio;
-  const bool grad_bf16 = a.grad_bf16 != 0;
   const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
   const float ce = a.entropy_cost;
   const int nchunks = static_cast<int>((T + kL - 1) / kL);
+  // Byte strides of one time row and the byte size of a chunk's 16 rows, per
+  // array (the host checks that these windows fit 32-bit offsets).
+  constexpr uint32_t gsz = kBf16Grad ? 2u : 4u;
+  const uint32_t row_h = static_cast<uint32_t>(B * H * 2);
+  const uint32_t row_d = static_cast<uint32_t>(B * H) * gsz;
+  const uint32_t row_s = static_cast<uint32_t>(B * 4);
+  const uint32_t row_y = static_cast<uint32_t>(B * A * sizeof(BehIn));
+  const uint32_t row_o = static_cast<uint32_t>(B * A1 * 4);
+  // A descriptor over a chunk's rows of a [T, B, n] array, starting at lane
+  // b of the chunk's first existing row and cut at the array's end, so that
+  // no offset it accepts lies outside the array.
+  auto chunk_rsrc = [&](const void* arr, int64_t n, int64_t elem_bytes, int64_t brow, bool on) {
+    const int64_t begin = brow * n * elem_bytes;
+    int64_t bytes = static_cast<int64_t>(kL) * B * n * elem_bytes;
+    const int64_t left = T * B * n * elem_bytes - begin;
+    bytes = bytes < left ? bytes : left;
+    return make_rsrc(static_cast<const char*>(arr) + (on ? begin : 0), on ? static_cast<uint32_t>(bytes) : 0u);
+  };
   const int64_t nquads = (B + kHeadWaves - 1) / kHeadWaves;
 
   f32x4 acc_w[S::MW][NT];
-  f32x4 acc_b[NT];
   static_for<NT>([&](auto CT) {
     constexpr int ct = decltype(CT)::value;
-    acc_b[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     static_for<S::MW>([&](auto MI) { acc_w[decltype(MI)::value][ct] = f32x4{0.f, 0.f, 0.f, 0.f}; });
   });
   double wave_pg = 0.0, wave_base = 0.0, wave_ent = 0.0;
@@ -177,6 +221,7 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
     const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
     double cy_V = boot, cy_v = boot, cy_A = 0.0;
     double l_pg = 0.0, l_base = 0.0, l_ent = 0.0;
+    bool bad_action = false;
 
     // Register prefetch of one chunk: this lane's hidden slice, behaviour
     // values and per-step scalars.
@@ -184,36 +229,53 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
     float yreg[NT][4];
     int32_t p_act = 0;
     float p_r = 0.f, p_g = 0.f, p_lmu = 0.f;
+    // Descriptors of a chunk start at its first existing row (wave-uniform);
+    // lane s of the row group reads row t0 + s at offset rel * row stride.
     auto prefetch = [&](int k) {
-      int64_t t = T - static_cast<int64_t>(k + 1) * kL + s;
-      t = t < 0 ? 0 : t;  // rows before t = 0 reread row 0 and are masked later
-      const int64_t row = t * B + (lane_ok ? b : 0);
-      const uint16_t* hp = a.hidden + row * H + 8 * g;
+      const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+      const int64_t tb = t0 < 0 ? 0 : t0;
+      const bool row_ok = t0 + s >= 0;
+      const uint32_t rel = static_cast<uint32_t>(t0 + s - tb);
+      const int64_t brow = tb * B + b;
+      const Rsrc rh = chunk_rsrc(a.hidden, H, 2, brow, lane_ok);
+      const uint32_t oh = row_ok ? rel * row_h + 16u * g : kOutOfRange;
       static_for<S::KS>([&](auto J) {
         constexpr int j = decltype(J)::value;
-        hreg[j] = lane_ok ? *reinterpret_cast<const v4u*>(hp + 32 * j) : v4u{0u, 0u, 0u, 0u};
+        hreg[j] = __builtin_bit_cast(v4u, __builtin_amdgcn_raw_buffer_load_b128(rh, oh + 64 * j, 0, 0));
       });
-      if (lane_ok) {
-        p_act = a.actions[row];
-        p_r = a.rewards[row];
-        p_g = a.discounts[row];
-        if (beh_lp && !no_ratio) p_lmu = static_cast<const float*>(a.behaviour)[row];
-      }
+      const uint32_t os = row_ok ? rel * row_s : kOutOfRange;
+      p_act = static_cast<int32_t>(
+          __builtin_amdgcn_raw_buffer_load_b32(chunk_rsrc(a.actions, 1, 4, brow, lane_ok), os, 0, 0));
+      p_r = buffer_load_f32(chunk_rsrc(a.rewards, 1, 4, brow, lane_ok), os);
+      p_g = buffer_load_f32(chunk_rsrc(a.discounts, 1, 4, brow, lane_ok), os);
+      p_lmu = buffer_load_f32(chunk_rsrc(a.behaviour, 1, 4, brow, lane_ok && beh_lp && !no_ratio), os);
+      // Behaviour logits: one offset per lane, the columns in the instruction
+      // offset.  Columns >= A read the next lane's row (or nothing, past the
+      // array's end); the epilogue only uses columns < A.
+      const Rsrc ry = chunk_rsrc(a.behaviour, A, sizeof(BehIn), brow, lane_ok && use_y);
+      const uint32_t oy = row_ok ? rel * row_y + 4u * g * static_cast<uint32_t>(sizeof(BehIn)) : kOutOfRange;
       static_for<NT>([&](auto CT) {
         constexpr int ct = decltype(CT)::value;
-        for (int i = 0; i < 4; ++i) {
-          const int c = 16 * ct + 4 * g + i;
-          yreg[ct][i] = (use_y && lane_ok && c < A) ? load_behaviour<BehIn>(a.behaviour, row * A + c) : 0.f;
-        }
+        static_for<4>([&](auto I) {
+          constexpr int i = decltype(I)::value;
+          yreg[ct][i] = buffer_load_logit<BehIn>(ry, oy + (16 * ct + i) * sizeof(BehIn));
+        });
       });
     };
 
     prefetch(0);
+    // Wait for the first chunk here, once per lane: the loop's first use of
+    // the prefetched registers is then reached from the loop entry with
+    // nothing outstanding, and the compiler's wait there only has to cover
+    // the previous iteration's loads, not the stores issued after them.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     for (int k = 0; k < nchunks; ++k) {
       const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
       const int64_t t = t0 + s;
       const bool step_ok = lane_ok && t >= 0;
-      const int64_t row = t * B + b;
+      const int64_t tb = t0 < 0 ? 0 : t0;
+      const uint32_t rel = static_cast<uint32_t>(t - tb);
+      const int64_t brow = tb * B + b;
 
       // 1. Forward product, from the prefetched hidden slice.
       f32x4 oacc[NT];
@@ -241,45 +303,68 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
       int32_t act = p_act;
       float r32 = p_r, g32 = p_g;
       const float lmu = p_lmu;
-      float y[NT][4];
-      static_for<NT>([&](auto CT) {
-        constexpr int ct = decltype(CT)::value;
-        for (int i = 0; i < 4; ++i) y[ct][i] = yreg[ct][i];
-      });
-      if (k + 1 < nchunks) prefetch(k + 1);
-
-      // 2. Epilogue.
-      r32 = transform_reward(r32, a.reward_transform);
-      if (!step_ok) act = 0;
+      if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
       const bool act_ok = act >= 0 && act < A;
       const int act_c = act_ok ? act : 0;
-      if (!act_ok) raise_error_flag(a.error_flag);
-
-      float o[NT][4];
-      float zmax = -INFINITY, ymax = -INFINITY, vloc = 0.f, zaloc = 0.f, yaloc = 0.f;
-      static_for<NT>([&](auto CT) {
-        constexpr int ct = decltype(CT)::value;
-        for (int i = 0; i < 4; ++i) {
-          const int c = 16 * ct + 4 * g + i;
-          o[ct][i] = oacc[ct][i] + bias[ct][i];
-          if (c < A) {
-            zmax = fmaxf(zmax, o[ct][i]);
-            ymax = fmaxf(ymax, y[ct][i]);
-          }
-          if (c == A) vloc = o[ct][i];
-          if (c == act_c) {
-            zaloc = o[ct][i];
-            yaloc = y[ct][i];
-          }
-        }
-      });
-      if (a.outputs != nullptr && step_ok) {
+      bad_action = bad_action || !act_ok;
+      // Behaviour-policy statistics of the step, taken before the prefetch
+      // below reuses their registers: m_y = max_j y_j, s_y = sum_j exp(y_j - m_y)
+      // and y_a.
+      using SumT = std::conditional_t<kPrecise, double, float>;
+      float my = 0.f, ya = 0.f;
+      SumT sy = 0;
+      if (use_y) {
+        float ymax = -INFINITY, yal = 0.f;
         static_for<NT>([&](auto CT) {
           constexpr int ct = decltype(CT)::value;
           for (int i = 0; i < 4; ++i) {
             const int c = 16 * ct + 4 * g + i;
-            if (c < A1) a.outputs[row * A1 + c] = o[ct][i];
+            if (c < A) ymax = fmaxf(ymax, yreg[ct][i]);
+            if (c == act_c) yal = yreg[ct][i];
           }
+        });
+        my = group_max(ymax);
+        ya = group_sum(yal);
+        SumT syl = 0;
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          for (int i = 0; i < 4; ++i) {
+            if (16 * ct + 4 * g + i < A) {
+              if constexpr (kPrecise)
+                syl += exp_nonpos_f64(static_cast<double>(yreg[ct][i]) - static_cast<double>(my));
+              else
+                syl += exp_fast(yreg[ct][i] - my);
+            }
+          }
+        });
+        sy = group_sum(syl);
+      }
+      if (k + 1 < nchunks) prefetch(k + 1);
+
+      // 2. Epilogue.
+      r32 = transform_reward(r32, a.reward_transform);
+
+      float o[NT][4];
+      float zmax = -INFINITY, vloc = 0.f, zaloc = 0.f;
+      static_for<NT>([&](auto CT) {
+        constexpr int ct = decltype(CT)::value;
+        for (int i = 0; i < 4; ++i) {
+          const int c = 16 * ct + 4 * g + i;
+          o[ct][i] = oacc[ct][i] + s_bias[c];
+          if (c < A) zmax = fmaxf(zmax, o[ct][i]);
+          if (c == A) vloc = o[ct][i];
+          if (c == act_c) zaloc = o[ct][i];
+        }
+      });
+      {
+        const Rsrc ro = chunk_rsrc(a.outputs, A1, 4, brow, lane_ok && a.outputs);
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          static_for<4>([&](auto I) {
+            constexpr int i = decltype(I)::value;
+            const int c = 16 * ct + 4 * g + i;
+            buffer_store_f32(o[ct][i], ro, (step_ok && c < A1) ? rel * row_o + 4u * c : kOutOfRange);
+          });
         });
       }
       const float V32 = group_sum(vloc);
@@ -290,9 +375,8 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
       double ratio;
       float inv_s, log_s, one_minus_pa, e_a, ed;
       if constexpr (kPrecise) {
-        double szl = 0.0, syl = 0.0;
+        double szl = 0.0;
         float edl = 0.f;
-        const float my = use_y ? group_max(ymax) : 0.f;
         static_for<NT>([&](auto CT) {
           constexpr int ct = decltype(CT)::value;
           for (int i = 0; i < 4; ++i) {
@@ -304,7 +388,6 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
               szl += x;
               e[ct][i] = static_cast<float>(x);
               edl = fmaf(e[ct][i], static_cast<float>(d), edl);
-              if (use_y) syl += exp_nonpos_f64(static_cast<double>(y[ct][i]) - static_cast<double>(my));
             }
           }
         });
@@ -318,17 +401,14 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         } else if (beh_lp) {
           ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
         } else {
-          const double sy = group_sum(syl);
-          const double ya = static_cast<double>(group_sum(yaloc));
-          ratio = act_ok ? exp(dza - (ya - static_cast<double>(my))) * (sy * inv) : NAN;
+          ratio = act_ok ? exp(dza - (static_cast<double>(ya) - static_cast<double>(my))) * (sy * inv) : NAN;
         }
         inv_s = static_cast<float>(inv);
         log_s = static_cast<float>(log(sz));
         one_minus_pa = static_cast<float>((sz - ea) * inv);
         e_a = static_cast<float>(ea);
       } else {
-        float szl = 0.f, syl = 0.f, edl = 0.f;
-        const float my = use_y ? group_max(ymax) : 0.f;
+        float szl = 0.f, edl = 0.f;
         static_for<NT>([&](auto CT) {
           constexpr int ct = decltype(CT)::value;
           for (int i = 0; i < 4; ++i) {
@@ -339,7 +419,6 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
               e[ct][i] = exp_fast(d);
               szl += e[ct][i];
               edl = fmaf(e[ct][i], d, edl);
-              if (use_y) syl += exp_fast(y[ct][i] - my);
             }
           }
         });
@@ -353,8 +432,6 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         } else if (beh_lp) {
           ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - log_s - lmu)) : NAN;
         } else {
-          const float sy = group_sum(syl);
-          const float ya = group_sum(yaloc);
           ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
         }
         inv_s = inv;
@@ -392,9 +469,10 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
       cy_v = dpp_f64<kRowShr15>(v_t);
       cy_V = dpp_f64<kRowShr15>(V);
 
-      if (step_ok && g == 0) {
-        if (a.vs) a.vs[row] = static_cast<float>(v_t);
-        if (a.pg_adv) a.pg_adv[row] = static_cast<float>(adv);
+      {
+        const uint32_t o1 = (step_ok && g == 0) ? rel * row_s : kOutOfRange;
+        buffer_store_f32(static_cast<float>(v_t), chunk_rsrc(a.vs, 1, 4, brow, lane_ok && a.vs), o1);
+        buffer_store_f32(static_cast<float>(adv), chunk_rsrc(a.pg_adv, 1, 4, brow, lane_ok && a.pg_adv), o1);
       }
 
       // G = dL/do for this step: the policy-logit gradient of the plain loss
@@ -429,8 +507,32 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         l_ent += -static_cast<double>(Hent);
       }
 
-      // 3. d_hidden = G W^T.
+      // 3. d_hidden = G W^T.  For float32 output M tile i gives lane (s, g)
+      // units 16i + 4g .. +3 of its step's row (one 16-byte store); for
+      // bfloat16, M tiles 2p and 2p+1 give it units 32p + 8g .. +7 (packed
+      // into one 16-byte store).  Either way the four lane groups write 64
+      // contiguous bytes of each row per instruction.
       const int grow = (kL * w + s) * S::GL_PITCH;
+      const uint32_t od = step_ok ? rel * row_d : kOutOfRange;
+      const Rsrc rd = chunk_rsrc(a.d_hidden, H, gsz, brow, lane_ok);
+      // M row (hidden unit) that operand lane s supplies in M tile i.
+      auto m_row = [&](int i) {
+        return kBf16Grad ? 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4) : 16 * i + s;
+      };
+      f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+      auto store_dh = [&](f32x4 acc, int i) {
+        if constexpr (!kBf16Grad) {
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, acc), rd,
+                                                 od + 4u * (16u * i + 4u * g), 0, 0);
+        } else {
+          if (i % 2 == 1) {
+            const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
+                            pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
+            __builtin_amdgcn_raw_buffer_store_b128(pk, rd, od + 2u * (32u * (i / 2) + 8u * g), 0, 0);
+          }
+          prev = acc;
+        }
+      };
       if constexpr (NT == 2) {
         const f32x8 gf = {Gv[0][0], Gv[0][1], Gv[0][2], Gv[0][3],
                           Gv[1][0], Gv[1][1], Gv[1][2], Gv[1][3]};
@@ -441,24 +543,12 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         reinterpret_cast<uint2*>(s_ghi + grow + 16 + 4 * g)[0] = uint2{uhi.z, uhi.w};
         reinterpret_cast<uint2*>(s_glo + grow + 4 * g)[0] = uint2{ulo.x, ulo.y};
         reinterpret_cast<uint2*>(s_glo + grow + 16 + 4 * g)[0] = uint2{ulo.z, ulo.w};
-        f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = grad_bf16 ? 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4) : 16 * i + s;
-          const bf16x8 wv = *reinterpret_cast<const bf16x8*>(&s_wp[hrow * S::WP_PITCH + 8 * g]);
+          const bf16x8 wv = *reinterpret_cast<const bf16x8*>(&s_wp[m_row(i) * S::WP_PITCH + 8 * g]);
           f32x4 acc = mfma_k32(wv, ghi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k32(wv, glo, acc);
-          if (step_ok) {
-            if (!grad_bf16) {
-              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + 16 * i + 4 * g) = acc;
-            } else if (i % 2 == 1) {
-              const int64_t hcol = 32 * (i / 2) + 8 * g;
-              const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
-                              pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
-              *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
-            }
-          }
-          prev = acc;
+          store_dh(acc, i);
         });
       } else {
         const f32x4 gf = {Gv[0][0], Gv[0][1], Gv[0][2], Gv[0][3]};
@@ -467,29 +557,19 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         const s16x4 shi = __builtin_bit_cast(s16x4, ghi), slo = __builtin_bit_cast(s16x4, glo);
         reinterpret_cast<s16x4*>(s_ghi + grow + 4 * g)[0] = shi;
         reinterpret_cast<s16x4*>(s_glo + grow + 4 * g)[0] = slo;
-        f32x4 prev = {0.f, 0.f, 0.f, 0.f};
         static_for<S::MT>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          const int hrow = grad_bf16 ? 32 * (i / 2) + 8 * (s / 4) + 4 * (i % 2) + (s % 4) : 16 * i + s;
-          const s16x4 wv = *reinterpret_cast<const s16x4*>(&s_wp[hrow * S::WP_PITCH + 4 * g]);
+          const s16x4 wv = *reinterpret_cast<const s16x4*>(&s_wp[m_row(i) * S::WP_PITCH + 4 * g]);
           f32x4 acc = mfma_k16(wv, shi, f32x4{0.f, 0.f, 0.f, 0.f});
           acc = mfma_k16(wv, slo, acc);
-          if (step_ok) {
-            if (!grad_bf16) {
-              *reinterpret_cast<f32x4*>(static_cast<float*>(a.d_hidden) + row * H + 16 * i + 4 * g) = acc;
-            } else if (i % 2 == 1) {
-              const int64_t hcol = 32 * (i / 2) + 8 * g;
-              const v4u pk = {pack_bf16x2(prev[0], prev[1]), pack_bf16x2(prev[2], prev[3]),
-                              pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3])};
-              *reinterpret_cast<v4u*>(static_cast<uint16_t*>(a.d_hidden) + row * H + hcol) = pk;
-            }
-          }
-          prev = acc;
+          store_dh(acc, i);
         });
       }
 
       // 4. d_W and d_bias over the four lanes' tiles of this chunk.
       __syncthreads();
+      f32x4 db[NT];
+      static_for<NT>([&](auto CT) { db[decltype(CT)::value] = f32x4{0.f, 0.f, 0.f, 0.f}; });
       static_for<kHeadWaves>([&](auto QI) {
         constexpr int q = decltype(QI)::value;
         s16x4 bh[NT], bl[NT];
@@ -517,13 +597,23 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
           const s16x4 ones = {0x3F80, 0x3F80, 0x3F80, 0x3F80};  // bfloat16 1.0
           static_for<NT>([&](auto CT) {
             constexpr int ct = decltype(CT)::value;
-            acc_b[ct] = mfma_k16(ones, bh[ct], acc_b[ct]);
-            acc_b[ct] = mfma_k16(ones, bl[ct], acc_b[ct]);
+            db[ct] = mfma_k16(ones, bh[ct], db[ct]);
+            db[ct] = mfma_k16(ones, bl[ct], db[ct]);
           });
         }
       });
+      // Wave 0 adds the chunk's column sums to its running d_bias (one lane
+      // per column, so the order of additions is fixed).
+      if (w == 0 && g == 0) {
+        static_for<NT>([&](auto CT) {
+          constexpr int ct = decltype(CT)::value;
+          s_db[16 * ct + s] += db[ct][0];
+        });
+      }
       __syncthreads();
     }
+
+    if (bad_action) raise_error_flag(a.error_flag);
 
     // This lane's loss sums (lanes of group 0 hold them), in a fixed order.
 #pragma unroll
@@ -559,7 +649,7 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
   if (w == 0 && g == 0) {
     static_for<NT>([&](auto CT) {
       constexpr int ct = decltype(CT)::value;
-      part[H * C + 16 * ct + s] = acc_b[ct][0];
+      part[H * C + 16 * ct + s] = s_db[16 * ct + s];
     });
   }
   if (l == 0) {
@@ -628,13 +718,21 @@ __global__ __launch_bounds__(256) void head_finish_kernel(HeadArgs a, int C, int
   }
 }
 
-template <int H, int NT, typename BehIn>
-void launch_head_shape(const HeadArgs& a, hipStream_t st, unsigned nwg) {
+template <int H, int NT, typename BehIn, bool kBf16Grad>
+void launch_head_grad(const HeadArgs& a, hipStream_t st, unsigned nwg) {
   const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
   if (precise)
-    hipLaunchKernelGGL((head_kernel<H, NT, true, BehIn>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
+    hipLaunchKernelGGL((head_kernel<H, NT, true, BehIn, kBf16Grad>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
   else
-    hipLaunchKernelGGL((head_kernel<H, NT, false, BehIn>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
+    hipLaunchKernelGGL((head_kernel<H, NT, false, BehIn, kBf16Grad>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
+}
+
+template <int H, int NT, typename BehIn>
+void launch_head_shape(const HeadArgs& a, hipStream_t st, unsigned nwg) {
+  if (a.grad_bf16)
+    launch_head_grad<H, NT, BehIn, true>(a, st, nwg);
+  else
+    launch_head_grad<H, NT, BehIn, false>(a, st, nwg);
 }
 
 template <int H>

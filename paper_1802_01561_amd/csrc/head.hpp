@@ -52,6 +52,10 @@ constexpr int64_t kHeadMaxWorkgroups = 512;
 // Hidden sizes with a kernel instance, and the largest A (A + 1 output columns
 // fill at most two 16-column MFMA tiles).
 constexpr int64_t kHeadMaxActions = 31;
+// The kernel addresses a chunk's 16 time rows of one array through one buffer
+// descriptor with 32-bit offsets: 16 rows of B*H float32 must stay below
+// 0xFFFFF000 bytes, so B*H is at most this.
+constexpr int64_t kHeadMaxBatchTimesHidden = 0xFFFFF000LL / 64;
 bool head_hidden_supported(int64_t H);
 int64_t head_workgroups(int64_t B);
 // Workspace of the fused kernel: the 256-byte header, then float64 loss
