@@ -57,6 +57,10 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
+    ap.add_argument("--cold", action="store_true",
+                    help="write a 512 MB buffer before each timed call (outside its events) so "
+                         "that no input is left in the 256 MB Infinity Cache; for workloads "
+                         "smaller than the cache")
     ap.add_argument("--head", action="store_true",
                     help="time the fused output layer + V-trace call (stress shape, H=256)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -208,10 +212,11 @@ def cpu_model():
     return name
 
 
-def timed_calls(step, K, W, stream):
+def timed_calls(step, K, W, stream, flush=None):
     """W untimed calls, then K calls bracketed by synchronisations, each between
-    two HIP events on the launch stream.  Returns (per-call event ms, wall ms
-    per call)."""
+    two HIP events on the launch stream (``flush``, when given, runs before
+    each call, outside its events).  Returns (per-call event ms, wall ms per
+    call)."""
     import numpy as np
     import torch
     for _ in range(W):
@@ -222,6 +227,8 @@ def timed_calls(step, K, W, stream):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
+        if flush is not None:
+            flush()
         starts[i].record(stream)
         step()
         ends[i].record(stream)
@@ -342,7 +349,9 @@ def run_head(args):
             "T": T, "B": B, "A": A, "H": H, "seed": seed,
         },
         "kernel_ms_avg": avg_ms,
+        "kernel_ms_median": float(np.median(call_ms)),
         "kernel_ms_min": float(call_ms.min()),
+        "timing": "back-to-back calls; value from the wall clock of the timed region",
         "alg_bytes_per_launch": alg_bytes,
         "alg_bytes_per_step": per_step,
         "traffic_bytes_per_launch": traffic_bytes,
@@ -422,7 +431,15 @@ def main():
                             reward_transform=args.reward_transform, grad_dtype=grad_dtype)
 
     K = args.steps
-    kernel_ms, ms_per_step = timed_calls(step, K, args.warmup, stream)
+    flush = None
+    if args.cold:
+        flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        flush = lambda: flush_buf.fill_(1)  # noqa: E731
+    kernel_ms, ms_per_step = timed_calls(step, K, args.warmup, stream, flush)
+    if args.cold:
+        # the wall clock includes the flushes: the cold rate comes from the
+        # events around each call alone
+        ms_per_step = float(np.median(kernel_ms))
     steps_per_s = T * B / (ms_per_step * 1e-3)
     logit_bytes = 2 if args.bf16 else 4
     alg_bytes, per_step = algorithmic_bytes(T, B, A, logit_bytes, args.log_probs,
@@ -467,6 +484,10 @@ def main():
             "seed": tr.seed,
         },
         "kernel_ms_avg": avg_kernel_ms,
+        "kernel_ms_median": float(np.median(kernel_ms)),
+        "timing": ("cold: a 512 MB buffer is written before each call; value from the median "
+                   "event time of the calls" if args.cold else
+                   "back-to-back calls; value from the wall clock of the timed region"),
         "alg_bytes_per_launch": alg_bytes,
         "traffic_bytes_per_launch": traffic_bytes,
         "kernel_ms_min": float(kernel_ms.min()),

@@ -672,12 +672,14 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
   }
 }
 
-// Adds the workgroups' partial sums in workgroup order (float64): d_W, d_bias
-// and the loss totals.  Block i covers 64 outputs; its four waves each sum a
-// quarter of the workgroups, and the quarters are added in order.
+// Adds the workgroups' partial sums in a fixed order (float64): d_W, d_bias and
+// the loss totals.  Block i covers 64 outputs; each of its 16 waves sums the
+// workgroups k = wave, wave + 16, ... (one coalesced 256-byte row per step),
+// and the 16 wave sums are added in wave order.
 constexpr int kFinishOutputs = 64;
-__global__ __launch_bounds__(256) void head_finish_kernel(HeadArgs a, int C, int nwg) {
-  __shared__ double s_q[4][kFinishOutputs];
+constexpr int kFinishWaves = 16;
+__global__ __launch_bounds__(kFinishWaves* kWave) void head_finish_kernel(HeadArgs a, int C, int nwg) {
+  __shared__ double s_q[kFinishWaves][kFinishOutputs];
   const int64_t H = a.H;
   const int A1 = static_cast<int>(a.A) + 1;
   const int64_t n_w = H * A1;
@@ -690,15 +692,14 @@ __global__ __launch_bounds__(256) void head_finish_kernel(HeadArgs a, int C, int
     off = static_cast<size_t>(i / A1) * C + static_cast<size_t>(i % A1);
   else if (i < n_out)
     off = static_cast<size_t>(H) * C + static_cast<size_t>(i - n_w);
-  const int per = (nwg + 3) / 4;
-  const int w0 = wv * per, w1 = (w0 + per < nwg) ? w0 + per : nwg;
   double sum = 0.0;
   if (i < n_out)
-    for (int k = w0; k < w1; ++k) sum += static_cast<double>(a.grad_partials[k * stride + off]);
+    for (int k = wv; k < nwg; k += kFinishWaves) sum += static_cast<double>(a.grad_partials[k * stride + off]);
   s_q[wv][lane] = sum;
   __syncthreads();
   if (wv == 0 && i < n_out) {
-    const double tot = ((s_q[0][lane] + s_q[1][lane]) + s_q[2][lane]) + s_q[3][lane];
+    double tot = 0.0;
+    for (int q = 0; q < kFinishWaves; ++q) tot += s_q[q][lane];
     if (i < n_w)
       a.d_weight[i] = static_cast<float>(tot);
     else
@@ -789,7 +790,7 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   const int64_t n_out = a.H * (a.A + 1) + (a.A + 1);
   const unsigned fb = static_cast<unsigned>((n_out + kFinishOutputs - 1) / kFinishOutputs);
-  hipLaunchKernelGGL(head_finish_kernel, dim3(fb), dim3(256), 0, st, a, head_columns(a.A),
+  hipLaunchKernelGGL(head_finish_kernel, dim3(fb), dim3(kFinishWaves * kWave), 0, st, a, head_columns(a.A),
                      static_cast<int>(nwg));
   return hipGetLastError();
 }
