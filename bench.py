@@ -47,7 +47,8 @@ def parse_args():
     ap.add_argument("--config", type=int, default=4, help="synthetic workload id (0-4)")
     ap.add_argument("--params", type=int, default=0, help="parameter set of the workload")
     ap.add_argument("--bf16", action="store_true", help="bfloat16 logits")
-    ap.add_argument("--kernel", choices=["auto", "lane_serial"], default="auto")
+    ap.add_argument("--kernel", choices=["auto", "lane_serial", "tiled", "wide"], default="auto",
+                    help="force one V-trace kernel (where it applies)")
     ap.add_argument("--correction", choices=["vtrace", "none", "epsilon", "one_step_is"],
                     default="vtrace")
     ap.add_argument("--log-probs", action="store_true",
@@ -380,8 +381,8 @@ def main():
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy, max(1, args.steps))
         return
-    if args.kernel == "lane_serial":
-        os.environ["VTRACE_KERNEL"] = "lane_serial"
+    if args.kernel != "auto":
+        os.environ["VTRACE_KERNEL"] = args.kernel
     if args.head:
         import torch
         if not torch.cuda.is_available():

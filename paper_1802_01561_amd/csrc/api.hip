@@ -42,11 +42,27 @@ bool dtype_of(vtrace_dtype d, LogitsType* lt) {
   return false;
 }
 
-// Kernel choice: the tiled kernel where it applies, else the generic one.
-// VTRACE_KERNEL=lane_serial forces the generic kernel (used to cross-check the two).
-bool force_lane_serial() {
+// Kernel choice: the time-parallel kernel for short unrolls of small batches,
+// the tiled kernel where it applies, else the generic one.  VTRACE_KERNEL
+// (lane_serial, tiled or wide) forces a kernel where it applies, to
+// cross-check them.
+enum class Kernel { Auto, LaneSerial, Tiled, Wide };
+Kernel forced_kernel() {
   const char* k = std::getenv("VTRACE_KERNEL");
-  return k != nullptr && std::strcmp(k, "lane_serial") == 0;
+  if (k == nullptr) return Kernel::Auto;
+  if (std::strcmp(k, "lane_serial") == 0) return Kernel::LaneSerial;
+  if (std::strcmp(k, "tiled") == 0) return Kernel::Tiled;
+  if (std::strcmp(k, "wide") == 0) return Kernel::Wide;
+  return Kernel::Auto;
+}
+
+// Where both apply, the time-parallel kernel wins while the tiled kernel's
+// serial walk over T / 16 chunks takes longer than the time-parallel kernel's
+// uncoalesced row reads: measured on MI355X (A = 9 and 18, T from 20 to 256,
+// B from 8 to 2048), that is for more than two chunks and B <= 128, or B <= 512
+// with T <= 100.  (The DMLab-shaped batch, T = 100 and B = 32, takes it.)
+bool prefer_wide(const StepArgs& a) {
+  return a.T > 32 && a.T <= 256 && (a.B <= 128 || (a.B <= 512 && a.T <= 100));
 }
 
 size_t workspace_bytes_for(int64_t B) {
@@ -155,7 +171,14 @@ vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s)
   (void)hipGetLastError();  // do not report an earlier, unrelated error
   int64_t nwg = 0;
   hipError_t e;
-  if (!force_lane_serial() && vtrace::tiled_supported(a, lt))
+  const Kernel k = forced_kernel();
+  const bool wide = vtrace::wide_supported(a, lt);
+  const bool tiled = vtrace::tiled_supported(a, lt);
+  if (k == Kernel::LaneSerial)
+    e = vtrace::launch_lane_serial(a, lt, mode, s, &nwg);
+  else if (wide && (k == Kernel::Wide || (k == Kernel::Auto && prefer_wide(a))))
+    e = vtrace::launch_wide(a, lt, mode, s, &nwg);
+  else if (tiled)
     e = vtrace::launch_tiled(a, lt, mode, s, &nwg);
   else
     e = vtrace::launch_lane_serial(a, lt, mode, s, &nwg);

@@ -49,8 +49,9 @@ constexpr size_t kWsHeaderBytes = 256;
 constexpr size_t kWsTicketOffset = 0;
 constexpr size_t kWsFlagOffset = 4;
 // Every loss kernel covers at least this many lanes per workgroup, so the
-// partials array is sized by ceil(B / kMinLanesPerWorkgroup).
-constexpr int64_t kMinLanesPerWorkgroup = 4;
+// partials array is sized by ceil(B / kMinLanesPerWorkgroup).  (The
+// time-parallel kernel holds a single lane per workgroup for T > 128.)
+constexpr int64_t kMinLanesPerWorkgroup = 1;
 
 enum class LogitsType { F32, BF16 };
 enum class Mode { Targets, LossGrad };
@@ -61,6 +62,9 @@ hipError_t launch_lane_serial(const StepArgs& a, LogitsType lt, Mode mode, hipSt
 bool tiled_supported(const StepArgs& a, LogitsType lt);
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                         int64_t* num_workgroups);
+bool wide_supported(const StepArgs& a, LogitsType lt);
+hipError_t launch_wide(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                       int64_t* num_workgroups);
 hipError_t launch_gather(int64_t T, int64_t B, int64_t A, LogitsType lt, const void* target,
                          const void* behaviour, const int32_t* actions, void* gathered,
                          hipStream_t s);

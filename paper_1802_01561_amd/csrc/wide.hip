@@ -1,0 +1,229 @@
+// Time-parallel V-trace kernel for short unrolls (T <= 256): one thread per
+// (lane, step), so a batch of B lanes runs its T steps at once instead of
+// walking 16-step chunks one after another.  This is the shape of the paper's
+// learner batches (B = 32 trajectories of 100 or 20 steps), where the chunk
+// walk leaves the GPU idle and the call is latency-bound.
+//
+// A workgroup of 256 threads holds 256 / TP lanes of TP steps each, TP the
+// power of two >= max(T, 16); thread (lane, t) handles step t, and the 16
+// consecutive steps of one DPP row never straddle two lanes.  The reverse
+// recursion v_t - V(x_t) = delta_t + gamma_t c_t (v_{t+1} - V(x_{t+1}))
+// (Remark 1) is an affine map per step; it is composed in two levels:
+//  1. a DPP suffix scan within each row of 16 steps (as in the tiled kernel);
+//  2. the rows' composites go through LDS, where one thread per lane walks its
+//     TP / 16 rows from the last and leaves each row the value at the next
+//     row's first step; applying it finishes every step.
+// Steps at or beyond T carry the identity-breaking map (0, 0), which makes
+// v_{T-1} use V(x_T) exactly as Eq. (1) does.  Each thread reads its own logit
+// rows straight from global memory: at these sizes latency, not bandwidth,
+// sets the time.
+#include "device_common.hpp"
+#include "row_stats.hpp"
+#include "wave_ops.hpp"
+
+namespace vtrace {
+namespace {
+
+constexpr int kWideThreads = 256;
+constexpr int kRow = 16;
+constexpr int kRows = kWideThreads / kRow;
+
+template <int A_, typename In, bool kGrad, bool kPrecise>
+__global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_log2) {
+  __shared__ double s_x[kWideThreads];    // V(x_t), then v_t, by thread
+  __shared__ double s_g[kRows], s_d[kRows], s_c[kRows];
+  __shared__ double s_loss[3 * kRows];
+  __shared__ double red_scratch[3 * (kWideThreads / kWave)];
+
+  const int tp = 1 << tp_log2;
+  const int tid = threadIdx.x;
+  const int lane_local = tid >> tp_log2;
+  const int t = tid & (tp - 1);
+  const int s = tid % kRow;
+  const int row = tid / kRow;
+  const int rows_per_lane = tp / kRow;
+  const int lanes = kWideThreads >> tp_log2;
+  const int64_t T = a.T, B = a.B;
+  const int64_t b = static_cast<int64_t>(blockIdx.x) * lanes + lane_local;
+  const bool lane_ok = b < B;
+  const bool step_ok = lane_ok && t < T;
+  const int64_t idx = step_ok ? static_cast<int64_t>(t) * B + b : 0;  // element 0 stands in
+
+  const bool beh_lp = a.behaviour_log_probs != 0;
+  const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
+  int32_t act = step_ok ? a.actions[idx] : 0;
+  float r32 = step_ok ? a.rewards[idx] : 0.f;
+  const float g32 = step_ok ? a.discounts[idx] : 0.f;
+  const float V32 = step_ok ? a.values[idx] : 0.f;
+  const float lmu = (step_ok && beh_lp && !no_ratio) ? static_cast<const float*>(a.behaviour_logits)[idx] : 0.f;
+  r32 = transform_reward(r32, a.reward_transform);
+  const bool act_ok = act >= 0 && act < A_;
+  const int act_c = act_ok ? act : 0;
+  if (step_ok && !act_ok) raise_error_flag(a.error_flag);
+
+  const In* zr = static_cast<const In*>(a.target_logits) + idx * A_;
+  const In* yr = static_cast<const In*>(a.behaviour_logits) + idx * A_;
+  float e[A_];
+  const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
+  const double lam = a.lambda;
+  const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, static_cast<double>(a.rho_bar)),
+                                        lam * clip_above(st.ratio, static_cast<double>(a.c_bar)), lam, act_ok);
+
+  const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
+  const double r = r32, gm = g32, V = V32;
+  const bool last = t == T - 1;
+  s_x[tid] = V;
+  __syncthreads();
+  const double V_next = last ? boot : (t + 1 < tp ? s_x[tid + 1] : 0.0);
+
+  // 1. Suffix scan of the affine maps within the row.
+  double G = step_ok ? gm * w.c_v : 0.0;
+  double D = step_ok ? w.rho_v * (r + gm * V_next - V) : 0.0;
+  static_for<4>([&](auto I) {
+    constexpr int off = 1 << decltype(I)::value;
+    const double Gn = dpp_f64<0x100 + off>(G);
+    const double Dn = dpp_f64<0x100 + off>(D);
+    if (s + off < kRow) {
+      D = fma(G, Dn, D);
+      G = G * Gn;
+    }
+  });
+  if (s == 0) {
+    s_g[row] = G;
+    s_d[row] = D;
+  }
+  __syncthreads();
+  // 2. Carries between the rows of a lane, from its last row backwards.
+  if (t == 0) {
+    double carry = 0.0;  // v - V just past the lane's last thread: beyond T, zero
+    for (int rr = rows_per_lane - 1; rr >= 0; --rr) {
+      s_c[row + rr] = carry;
+      carry = fma(s_g[row + rr], carry, s_d[row + rr]);
+    }
+  }
+  __syncthreads();
+  const double A_t = fma(G, s_c[row], D);  // v_t - V(x_t)
+  const double v_t = V + A_t;
+  s_x[tid] = v_t;
+  __syncthreads();
+  const double v_next = last ? boot : (t + 1 < tp ? s_x[tid + 1] : 0.0);
+  const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+  const double adv = w.rho_pg * (r + gm * q_next - V);
+
+  if (step_ok) {
+    if (a.vs) a.vs[idx] = static_cast<float>(v_t);
+    if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+  }
+
+  if constexpr (kGrad) {
+    // d_logits_j = adv (pi_j - 1[j=a]) + ce pi_j (log pi_j + H): e_j (alpha +
+    // beta z_j) off the taken action, as in the tiled kernel.
+    const float ce = a.entropy_cost;
+    const float K = st.mz + st.log_s - st.H;
+    const float pa = st.e_a * st.inv_s;
+    const bool eps_mode = a.correction == kCorrEpsilon;
+    const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
+    const float adv32 = static_cast<float>(adv) * pg_w;
+    const float beta = st.inv_s * ce;
+    const float alpha = st.inv_s * adv32 - beta * K;
+    const float za = logit_to_float(zr[act_c]);
+    const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
+    double l_pg = 0.0, l_base = 0.0, l_ent = 0.0;
+    if (step_ok) {
+      a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+      const double log_pa =
+          !act_ok ? NAN
+          : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
+                     : static_cast<double>(za - st.mz) - static_cast<double>(st.log_s);
+      l_pg = -adv * log_pa;
+      l_base = 0.5 * A_t * A_t;
+      l_ent = -static_cast<double>(st.H);
+      const bool bf16 = a.grad_bf16 != 0;
+#pragma unroll
+      for (int j = 0; j < A_; ++j) {
+        float x = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
+        if (j == act_c) x = act_ok ? out_a : NAN;
+        if (bf16)
+          static_cast<uint16_t*>(a.d_logits)[idx * A_ + j] = to_bf16(x);
+        else
+          static_cast<float*>(a.d_logits)[idx * A_ + j] = x;
+      }
+    }
+    // Loss sums: per row (fixed butterfly), per lane (rows in order), then
+    // over the batch.
+#pragma unroll
+    for (int off = kRow / 2; off > 0; off >>= 1) {
+      l_pg += __shfl_xor(l_pg, off, kRow);
+      l_base += __shfl_xor(l_base, off, kRow);
+      l_ent += __shfl_xor(l_ent, off, kRow);
+    }
+    if (s == 0) {
+      s_loss[3 * row + 0] = l_pg;
+      s_loss[3 * row + 1] = l_base;
+      s_loss[3 * row + 2] = l_ent;
+    }
+    __syncthreads();
+    double pg = 0.0, base = 0.0, ent = 0.0;
+    if (t == 0) {
+      for (int rr = 0; rr < rows_per_lane; ++rr) {
+        pg += s_loss[3 * (row + rr) + 0];
+        base += s_loss[3 * (row + rr) + 1];
+        ent += s_loss[3 * (row + rr) + 2];
+      }
+      base *= a.baseline_cost;
+      ent *= a.entropy_cost;
+      if (lane_ok && a.lane_losses) {
+        a.lane_losses[3 * b + 0] = static_cast<float>(pg);
+        a.lane_losses[3 * b + 1] = static_cast<float>(base);
+        a.lane_losses[3 * b + 2] = static_cast<float>(ent);
+      }
+      if (!lane_ok) pg = base = ent = 0.0;
+    }
+    finish_losses<kWideThreads>(a, pg, base, ent, red_scratch);
+  }
+}
+
+template <int A_, typename In, bool kGrad>
+void launch_wide_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int tp_log2) {
+  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+  if (precise)
+    hipLaunchKernelGGL((wide_kernel<A_, In, kGrad, true>), dim3(blocks), dim3(kWideThreads), 0, st, a,
+                       tp_log2);
+  else
+    hipLaunchKernelGGL((wide_kernel<A_, In, kGrad, false>), dim3(blocks), dim3(kWideThreads), 0, st, a,
+                       tp_log2);
+}
+
+template <int A_, typename In>
+hipError_t launch_wide_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg) {
+  int tp_log2 = 4;
+  while ((int64_t(1) << tp_log2) < a.T) ++tp_log2;
+  const int64_t lanes = kWideThreads >> tp_log2;
+  const int64_t blocks = (a.B + lanes - 1) / lanes;
+  *nwg = blocks;
+  if (mode == Mode::LossGrad)
+    launch_wide_mode<A_, In, true>(a, st, static_cast<unsigned>(blocks), tp_log2);
+  else
+    launch_wide_mode<A_, In, false>(a, st, static_cast<unsigned>(blocks), tp_log2);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool wide_supported(const StepArgs& a, LogitsType) {
+  return (a.A == 9 || a.A == 18) && a.T <= kWideThreads && a.B <= (int64_t(1) << 31);
+}
+
+hipError_t launch_wide(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
+                       int64_t* num_workgroups) {
+  if (lt == LogitsType::F32) {
+    if (a.A == 18) return launch_wide_shape<18, float>(a, mode, st, num_workgroups);
+    if (a.A == 9) return launch_wide_shape<9, float>(a, mode, st, num_workgroups);
+  } else {
+    if (a.A == 18) return launch_wide_shape<18, uint16_t>(a, mode, st, num_workgroups);
+    if (a.A == 9) return launch_wide_shape<9, uint16_t>(a, mode, st, num_workgroups);
+  }
+  return hipErrorNotSupported;
+}
+
+}  // namespace vtrace

@@ -252,29 +252,62 @@ def test_gradient_invariants():
     assert np.all(np_out(out1.d_logits) == 0.0)
 
 
+@pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("pidx", [0, 1])
-def test_kernels_agree(monkeypatch, pidx):
-    """The tiled kernel and the generic lane-serial kernel give the same results:
-    tightly where every weight is at most 1 (nothing amplifies rounding), to the
-    oracle's tolerance where the weights are unclipped."""
+def test_kernels_agree(monkeypatch, pidx, kernel):
+    """The tiled and the time-parallel kernel each give the generic lane-serial
+    kernel's results: tightly where every weight is at most 1 (nothing
+    amplifies rounding), to the oracle's tolerance where the weights are
+    unclipped."""
     p = PARAM_SETS[4][pidx]
     tight = pidx == 0
     for (T, B, A, bf16) in [(100, 4096, 9, False), (60, 1000, 18, False), (50, 777, 9, True)]:
         tr = make_random(T, B, A, 31 + A, noise_std=1.0, bf16=bf16)
         dev = to_device(tr)
-        log_case(f"kernel agreement T={T} B={B} A={A} bf16={bf16} {p.label()}")
+        log_case(f"kernel agreement {kernel} T={T} B={B} A={A} bf16={bf16} {p.label()}")
+        monkeypatch.setenv("VTRACE_KERNEL", kernel)
         a = run_loss_grad(dev, p)
         monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
         b = run_loss_grad(dev, p)
         monkeypatch.delenv("VTRACE_KERNEL")
         for name in ("vs", "pg_advantages", "d_values", "d_logits"):
             kw = dict(rtol=2e-5, atol=2e-6) if tight else {}
-            assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
+            assert_close(f"{kernel} vs lane_serial {name}", np_out(getattr(a, name)),
                          np_out(getattr(b, name)), **kw)
         # loss sums cancel (advantages of both signs): the oracle's tolerance
         for name in ("lane_losses", "losses"):
-            assert_close(f"tiled vs lane_serial {name}", np_out(getattr(a, name)),
+            assert_close(f"{kernel} vs lane_serial {name}", np_out(getattr(a, name)),
                          np_out(getattr(b, name)))
+
+
+@pytest.mark.parametrize("kernel", ["tiled", "wide"])
+@pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
+                                      (2, True)])
+def test_config_each_kernel(cfg, bf16, kernel, monkeypatch):
+    """Configs 0-3 through each of the two fast kernels (the automatic choice
+    takes the time-parallel one for these shapes)."""
+    monkeypatch.setenv("VTRACE_KERNEL", kernel)
+    tr = make_config(cfg, bf16=bf16)
+    dev = to_device(tr)
+    for p in (PARAM_SETS[cfg][0], PARAM_SETS[4][1], PARAM_SETS[4][2]):
+        log_case(f"config {cfg} bf16={bf16} kernel={kernel} {p.label()}")
+        check_against_oracle(tr, p, run_loss_grad(dev, p))
+
+
+WIDE_SHAPES = [(1, 1, 9), (1, 300, 18), (16, 16, 18), (17, 7, 9), (31, 5, 18), (64, 9, 9),
+               (100, 33, 18), (128, 4, 9), (129, 3, 9), (200, 2, 18), (256, 3, 9), (255, 1, 18)]
+
+
+@pytest.mark.parametrize("T,B,A", WIDE_SHAPES)
+def test_wide_kernel_shapes(T, B, A, monkeypatch):
+    """The time-parallel kernel at every lane packing (T up to 16, 32, ..., 256:
+    16 to 1 lanes per workgroup), ragged T and B, fp32 and bf16 logits."""
+    monkeypatch.setenv("VTRACE_KERNEL", "wide")
+    for bf16 in (False, True):
+        tr = make_random(T, B, A, 2000 + T + B + A, noise_std=1.0, end_prob=0.05, bf16=bf16)
+        for p in (PARAM_SETS[4][0], PARAM_SETS[4][1]):
+            log_case(f"wide T={T} B={B} A={A} bf16={bf16} {p.label()}")
+            check_against_oracle(tr, p, run_loss_grad(to_device(tr), p))
 
 
 def test_offsets_beyond_two_gib():

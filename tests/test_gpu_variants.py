@@ -46,13 +46,15 @@ def check_variant(tr, p, correction, q_estimate, epsilon=1e-6):
     assert_close(f"{tag} targets.pg_advantages", np_out(pg), o.pg_advantages)
 
 
+@pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("correction", CORRECTIONS)
 @pytest.mark.parametrize("q_estimate", Q_ESTIMATES)
 @pytest.mark.parametrize("cfg", [1, 2])
-def test_variants_on_configs(cfg, correction, q_estimate):
+def test_variants_on_configs(cfg, correction, q_estimate, kernel, monkeypatch):
+    monkeypatch.setenv("VTRACE_KERNEL", kernel)
     tr = make_config(cfg)
     for p in (Params(1.0, 1.0, 1.0), Params(2.0, 1.0, 0.9), Params(math.inf, math.inf, 1.0)):
-        log_case(f"config {cfg} {correction}/{q_estimate} {p.label()}")
+        log_case(f"config {cfg} {correction}/{q_estimate} kernel={kernel} {p.label()}")
         check_variant(tr, p, correction, q_estimate)
 
 
@@ -160,10 +162,12 @@ def check_io_variant(tr, p, *, log_probs=False, reward_transform=None, grad_bf16
         assert_close(f"{tag} targets.pg_advantages", np_out(pg), o.pg_advantages)
 
 
+@pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("log_probs", [False, True])
 @pytest.mark.parametrize("reward_transform", [None, "clip", "asymmetric"])
 @pytest.mark.parametrize("grad_bf16", [False, True])
-def test_io_variants_configs(log_probs, reward_transform, grad_bf16):
+def test_io_variants_configs(log_probs, reward_transform, grad_bf16, kernel, monkeypatch):
+    monkeypatch.setenv("VTRACE_KERNEL", kernel)
     for cfg in (1, 2):
         tr = make_config(cfg)
         tr.rewards = (tr.rewards * 3.0 - 0.5).astype(np.float32)  # exercise the clipping
