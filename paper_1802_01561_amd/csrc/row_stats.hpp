@@ -46,14 +46,19 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
   st.mz = mz;
   float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
   if constexpr (kPrecise) {
+    // The exponent sums decide the ratio and are formed in float64; a short
+    // unroll keeps their float64 temporaries from crowding out the registers
+    // the rest of the step needs.  The e_j themselves only enter the gradient
+    // and the entropy, where float32 exponentials are accurate enough.
     double sz = 0.0, sy = 0.0;
+#pragma unroll 3
+    for (int j = 0; j < A_; ++j)
+      sz += exp_nonpos_f64(static_cast<double>(logit_to_float(zr[j])) - static_cast<double>(mz));
 #pragma unroll
     for (int j = 0; j < A_; ++j) {
-      const double d = static_cast<double>(logit_to_float(zr[j])) - static_cast<double>(mz);
-      const double x = exp_nonpos_f64(d);
-      sz += x;
-      e[j] = static_cast<float>(x);
-      ed = fmaf(e[j], static_cast<float>(d), ed);
+      const float d = logit_to_float(zr[j]) - mz;
+      e[j] = exp_fast(d);
+      ed = fmaf(e[j], d, ed);
     }
     const double inv = 1.0 / sz;
     const double dza = static_cast<double>(za) - static_cast<double>(mz);
@@ -63,7 +68,7 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
     } else if (beh_lp) {
       st.ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
     } else {
-#pragma unroll
+#pragma unroll 3
       for (int j = 0; j < A_; ++j)
         sy += exp_nonpos_f64(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
       const double dya = static_cast<double>(ya) - static_cast<double>(my);
