@@ -37,10 +37,13 @@
  *             (every v_s uses the rest of the unroll; v_T = V(x_T))
  *   pg_adv_s = rho_s (r_s + gamma_s v_{s+1} - V(x_s))
  *
- * Numerics.  Per-row softmax work is float32; the importance ratio is formed
- * in float64 from the float32 exponent sums, and the recursion, advantages and
- * loss partial sums are float64.  Outputs are float32.  NaN or Inf inputs are
- * propagated, not sanitised.
+ * Numerics.  Per-row softmax work is float32 and the recursion, advantages and
+ * loss partial sums are float64.  The importance ratio is formed from float32
+ * exponent sums while every weight is at most 1 (rho_bar <= 1 and
+ * lambda * c_bar <= 1, where nothing amplifies its rounding), and from float64
+ * exponentials and sums otherwise (V-trace with larger or no truncation, where
+ * products of c_t can grow).  Outputs are float32 (or bfloat16 where a variant
+ * asks for it).  NaN or Inf inputs are propagated, not sanitised.
  *
  * Errors that only the device can see.  An action outside [0, A) makes that
  * step's importance ratio NaN; the NaN reaches that step's outputs, every
