@@ -257,3 +257,21 @@ def test_head_variant_and_behaviour_alignment(L):
     assert _head(L, dt=1, beh=P + 2, T=0) == SHAPE
     assert _head(L, dt=1, beh=P + 1) == ALIGN
     assert _head(L, variant=ctypes.byref(V(0, 0, 0.0, 1, 0, 0)), beh=P + 2) == ALIGN
+
+
+def test_python_head_binding_validates_before_calling():
+    torch = pytest.importorskip("torch")
+    import paper_1802_01561_amd as v
+    T, B, A, H = 3, 2, 5, 64
+    h = torch.zeros(T, B, H, dtype=torch.bfloat16)
+    W = torch.zeros(H, A + 1, dtype=torch.bfloat16)
+    args = [h, W, torch.zeros(A + 1), torch.zeros(T, B, A), torch.zeros(T, B, dtype=torch.int32),
+            torch.zeros(T, B), torch.zeros(T, B), torch.zeros(B)]
+    with pytest.raises(ValueError):  # CPU tensors are refused before any device work
+        v.vtrace_head_loss_grad(*args)
+    with pytest.raises(ValueError):
+        v.vtrace_head_loss_grad(h[0], *args[1:])  # hidden must be [T, B, H]
+    with pytest.raises(ValueError):
+        v.vtrace_head_loss_grad(*args, correction="retrace")
+    with pytest.raises(ValueError):
+        v.vtrace_head_loss_grad(*args, grad_dtype=torch.float16)
