@@ -310,17 +310,21 @@ def test_wide_kernel_shapes(T, B, A, monkeypatch):
             check_against_oracle(tr, p, run_loss_grad(to_device(tr), p))
 
 
-def test_offsets_beyond_two_gib():
-    """Logit tensors larger than 2^31 bytes (T=64, B=524288, A=18: 2.4 GB each):
-    byte offsets need 64 bits; the oracle checks lanes spread over the batch,
-    including the last ones."""
-    T, B, A = 64, 1 << 19, 18
+def test_offsets_beyond_four_gib():
+    """Logit tensors larger than 2^32 bytes (T=64, B=2^20+8, A=18: 4.8 GB each):
+    byte offsets need more than 32 bits, signed or not.  Rows stay 16-byte
+    aligned, so all but the last, ragged workgroup take the vector path; the
+    oracle checks lanes spread over the batch, including the last ones, whose
+    elements lie beyond 2^32 bytes."""
+    T, B, A = 64, (1 << 20) + 8, 18
+    assert T * B * A * 4 > 2**32
     log_case(f"large batch T={T} B={B} A={A} ({T * B * A * 4 / 2**30:.2f} GiB per logit tensor)")
     tr = make_random(T, B, A, 4321, noise_std=1.0, end_prob=0.01)
     dev = to_device(tr)
-    lanes = sorted(set([0, 1, B // 2, B - 17, B - 2, B - 1] + list(range(B - 64, B, 7))))
+    lanes = sorted(set([0, 1, B // 2, B - 17, B - 9, B - 8, B - 2, B - 1] + list(range(B - 64, B, 7))))
     for p in (PARAM_SETS[4][0], PARAM_SETS[4][1]):
         out = run_loss_grad(dev, p)
         check_against_oracle(tr, p, out, lanes=lanes)
+        del out
     del dev
     torch.cuda.empty_cache()
