@@ -47,8 +47,10 @@ def parse_args():
     ap.add_argument("--config", type=int, default=4, help="synthetic workload id (0-4)")
     ap.add_argument("--params", type=int, default=0, help="parameter set of the workload")
     ap.add_argument("--bf16", action="store_true", help="bfloat16 logits")
-    ap.add_argument("--kernel", choices=["auto", "lane_serial", "tiled", "wide"], default="auto",
-                    help="force one V-trace kernel (where it applies)")
+    ap.add_argument("--kernel", choices=["auto", "lane_serial", "tiled", "tiled_single", "wide"],
+                    default="auto",
+                    help="force one V-trace kernel (where it applies); tiled_single keeps the tiled "
+                         "kernel to one workgroup per tile")
     ap.add_argument("--correction", choices=["vtrace", "none", "epsilon", "one_step_is"],
                     default="vtrace")
     ap.add_argument("--log-probs", action="store_true",

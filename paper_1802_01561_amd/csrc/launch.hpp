@@ -60,8 +60,9 @@ enum class Mode { Targets, LossGrad };
 hipError_t launch_lane_serial(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                               int64_t* num_workgroups);
 bool tiled_supported(const StepArgs& a, LogitsType lt);
+// allow_multi false keeps one workgroup per tile (no multi-tile walk).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
-                        int64_t* num_workgroups);
+                        int64_t* num_workgroups, bool allow_multi);
 bool wide_supported(const StepArgs& a, LogitsType lt);
 hipError_t launch_wide(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                        int64_t* num_workgroups);

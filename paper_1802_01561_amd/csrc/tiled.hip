@@ -1,11 +1,13 @@
 // Tiled V-trace kernel for the common action counts (A = 9: DeepMind Lab,
 // A = 18: the full Atari set).
 //
-// Work split.  A workgroup owns LANES consecutive lanes (batch entries) for the
-// whole unroll and walks time backwards in chunks of L = 16 steps, so every
-// carry of the reverse recursion stays inside the workgroup.  Within a chunk,
-// thread (lane, s) handles step t = t0 + s; the 16 threads of one lane are one
-// DPP row of a wave.
+// Work split.  A tile is LANES consecutive lanes (batch entries) for the whole
+// unroll; a workgroup walks a tile's time backwards in chunks of L = 16 steps,
+// so every carry of the reverse recursion stays inside the workgroup.  Within
+// a chunk, thread (lane, s) handles step t = t0 + s; the 16 threads of one lane
+// are one DPP row of a wave.  When the batch has a whole multiple of the tiles
+// the chip holds workgroups at once, each resident workgroup walks an equal
+// share of tiles as one continuous sequence of chunks.
 //
 // Data path per chunk.
 //  1. For each t the chunk's logits are one contiguous run of LANES*A elements
@@ -29,6 +31,9 @@
 // Workgroups whose lane tile is full and whose rows are 16-byte aligned take
 // the vector path above; a ragged last tile (or unaligned rows) copies element
 // by element without prefetching.
+#include <atomic>
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "row_stats.hpp"
 #include "wave_ops.hpp"
@@ -71,8 +76,16 @@ struct Carry {
 };
 
 
-template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kVec>
-__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t tile, Carry& cy) {
+// Walks one tile (kMulti false: `tile`, with the carry cy set up by the
+// caller), or (kMulti true, vector tiles only) the tiles first_tile + i *
+// tile_stride, i < ntiles, one after another as one loop over their chunks, so
+// that the prefetch runs across tile boundaries; each lane's loss totals are
+// then added to acc[3 * lane], a slot only the lane's step-0 thread touches.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kVec, bool kMulti>
+__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t first_tile,
+                                           int64_t tile_stride, int64_t ntiles, Carry& cy,
+                                           double* acc) {
+  static_assert(kVec || !kMulti, "the multi-tile walk takes vector tiles only");
   using S = Tile<A_, LANES, In>;
   constexpr int NT = S::NT;
   v4u* const lds_z = lds;
@@ -82,10 +95,6 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   const int lane_local = tid / kL;
   const int s = tid % kL;
   const int64_t T = a.T, B = a.B;
-  const int64_t b0 = tile * LANES;
-  const int64_t b = b0 + lane_local;
-  const bool lane_ok = b < B;
-  const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
   const int nchunks = static_cast<int>((T + kL - 1) / kL);
 
   // Byte stride of one time row of logits.
@@ -97,18 +106,21 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   const bool grad_bf16 = a.grad_bf16 != 0;
   const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
   const int64_t out_row = B * A_ * gsz;
-  const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
-  const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
   const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
-  char* const dg = static_cast<char*>(a.d_logits) + b0 * A_ * gsz;
 
   // Register prefetch (vector path): NV 16-byte vectors covering both tensors,
-  // plus this thread's action, reward, discount and value.
+  // plus this thread's action, reward, discount and value, and at a tile's
+  // first chunk its lane's bootstrap value.
   v4u pre[S::NV];
   int32_t p_act = 0;
-  float p_r = 0.f, p_g = 0.f, p_V = 0.f, p_lmu = 0.f;
+  float p_r = 0.f, p_g = 0.f, p_V = 0.f, p_lmu = 0.f, p_boot = 0.f;
 
-  auto prefetch = [&](int k) {
+  auto prefetch = [&](int64_t tile, int k) {
+    const int64_t b0 = tile * LANES;
+    const int64_t b = b0 + lane_local;
+    const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
+    const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
+    const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
     const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
     const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row 0
     static_for<S::NV>([&](auto I) {
@@ -134,14 +146,33 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       p_g = a.discounts[idx];
       p_V = a.values[idx];
       if (beh_lp && !no_ratio) p_lmu = lmu_g[idx];
+      if (kMulti && k == 0) p_boot = a.bootstrap_value[b];
     }
   };
 
   const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
   const float ce = a.entropy_cost;
 
-  if constexpr (kVec) prefetch(0);
-  for (int k = 0; k < nchunks; ++k) {
+  int64_t tile = first_tile;  // advanced by the multi-tile walk only
+  int k = 0;
+  // Chunks to walk: a tile's, or all the tiles' (which may exceed 32 bits).
+  using Count = std::conditional_t<kMulti, int64_t, int>;
+  const Count total = kMulti ? static_cast<Count>(ntiles * nchunks) : static_cast<Count>(nchunks);
+  if constexpr (kVec) prefetch(tile, 0);
+  for (Count it = 0; it < total; ++it) {
+    const int64_t b0 = tile * LANES;
+    const int64_t b = b0 + lane_local;
+    const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
+    const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
+    char* const dg = static_cast<char*>(a.d_logits) + b0 * A_ * gsz;
+    if constexpr (kMulti) {
+      if (k == 0) {
+        // A new tile: the carry past its last step is the bootstrap value
+        // (v_T = V(x_T), so v_T - V(x_T) = 0).
+        cy.V = cy.v = p_boot;
+        cy.A = 0.0;
+      }
+    }
     const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
     const int64_t t = t0 + s;
     const bool step_ok = lane_ok && t >= 0;
@@ -167,7 +198,14 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       V32 = p_V;
       lmu = p_lmu;
       __syncthreads();
-      if (k + 1 < nchunks) prefetch(k + 1);
+      if constexpr (kMulti) {
+        if (it + 1 < total) {
+          const bool next_tile = k + 1 == nchunks;
+          prefetch(next_tile ? tile + tile_stride : tile, next_tile ? 0 : k + 1);
+        }
+      } else {
+        if (k + 1 < nchunks) prefetch(tile, k + 1);
+      }
     } else {
       In* lz = reinterpret_cast<In*>(lds_z);
       In* ly = reinterpret_cast<In*>(lds_y);
@@ -322,78 +360,195 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
           }
         }
       }
+      if (kMulti && k == nchunks - 1) {
+        // The tile's last chunk: this lane's totals over the row (fixed
+        // butterfly order), then the workgroup's running sums.
+        double lp = cy.pg, lb = cy.base, le = cy.ent;
+#pragma unroll
+        for (int off = kL / 2; off > 0; off >>= 1) {
+          lp += __shfl_xor(lp, off, kL);
+          lb += __shfl_xor(lb, off, kL);
+          le += __shfl_xor(le, off, kL);
+        }
+        lb *= a.baseline_cost;
+        le *= a.entropy_cost;
+        if (s == 0 && lane_ok) {
+          if (a.lane_losses) {
+            a.lane_losses[3 * b + 0] = static_cast<float>(lp);
+            a.lane_losses[3 * b + 1] = static_cast<float>(lb);
+            a.lane_losses[3 * b + 2] = static_cast<float>(le);
+          }
+          acc[3 * lane_local + 0] += lp;
+          acc[3 * lane_local + 1] += lb;
+          acc[3 * lane_local + 2] += le;
+        }
+        cy.pg = cy.base = cy.ent = 0.0;
+      }
+    }
+    if (++k == nchunks && kMulti) {
+      k = 0;
+      tile += tile_stride;
     }
   }
 }
 
-template <int A_, int LANES, typename In, bool kGrad, bool kPrecise>
-__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t num_vec_tiles) {
+// kMulti false: one workgroup per tile, tile xcd_tile(blockIdx), which puts
+// workgroups that run side by side on one XCD on neighbouring tiles, whose
+// [T,B] scalars share 128-byte lines in that XCD's L2.
+//
+// kMulti true: the grid is exactly the workgroups the chip holds at once and
+// each walks tiles_per_wg vector tiles, xcd_tile(blockIdx) + i * gridDim.x.
+// When a batch has a whole multiple of that many tiles, this runs it as one
+// even generation: one workgroup per tile would instead start a second wave of
+// workgroups whenever a slot frees, and leave the chip partly idle at the end.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kMulti>
+__global__ __launch_bounds__(LANES* kL) void tiled_kernel(StepArgs a, int64_t num_vec_tiles,
+                                                          int64_t tiles_per_wg) {
   using S = Tile<A_, LANES, In>;
   constexpr int NT = S::NT;
   __shared__ v4u lds[S::LDS16];
   __shared__ double red_scratch[3 * (NT / kWave)];
 
-  const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
   const int lane_local = threadIdx.x / kL;
   const int s = threadIdx.x % kL;
-  const int64_t b = tile * LANES + lane_local;
-  const bool lane_ok = b < a.B;
-  const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
-  Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
 
-  if (tile < num_vec_tiles)
-    chunk_walk<A_, LANES, In, kGrad, kPrecise, true>(a, lds, tile, cy);
-  else
-    chunk_walk<A_, LANES, In, kGrad, kPrecise, false>(a, lds, tile, cy);
+  if constexpr (kMulti) {
+    __shared__ double acc[3 * LANES];  // per-lane loss sums over the workgroup's tiles
+    if (s == 0) acc[3 * lane_local + 0] = acc[3 * lane_local + 1] = acc[3 * lane_local + 2] = 0.0;
+    Carry cy{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    chunk_walk<A_, LANES, In, kGrad, kPrecise, true, true>(a, lds, xcd_tile(blockIdx.x, gridDim.x),
+                                                           gridDim.x, tiles_per_wg, cy, acc);
+    if constexpr (kGrad) {
+      double pg = 0.0, base = 0.0, ent = 0.0;
+      if (s == 0) {
+        pg = acc[3 * lane_local + 0];
+        base = acc[3 * lane_local + 1];
+        ent = acc[3 * lane_local + 2];
+      }
+      finish_losses<NT>(a, pg, base, ent, red_scratch);
+    }
+  } else {
+    const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int64_t b = tile * LANES + lane_local;
+    const bool lane_ok = b < a.B;
+    const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
+    Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
 
-  if constexpr (kGrad) {
-    // Per-lane totals over the row (fixed butterfly order), then the workgroup.
-    double pg = cy.pg, base = cy.base, ent = cy.ent;
+    if (tile < num_vec_tiles)
+      chunk_walk<A_, LANES, In, kGrad, kPrecise, true, false>(a, lds, tile, 0, 1, cy, nullptr);
+    else
+      chunk_walk<A_, LANES, In, kGrad, kPrecise, false, false>(a, lds, tile, 0, 1, cy, nullptr);
+
+    if constexpr (kGrad) {
+      // Per-lane totals over the row (fixed butterfly order), then the workgroup.
+      double pg = cy.pg, base = cy.base, ent = cy.ent;
 #pragma unroll
-    for (int off = kL / 2; off > 0; off >>= 1) {
-      pg += __shfl_xor(pg, off, kL);
-      base += __shfl_xor(base, off, kL);
-      ent += __shfl_xor(ent, off, kL);
+      for (int off = kL / 2; off > 0; off >>= 1) {
+        pg += __shfl_xor(pg, off, kL);
+        base += __shfl_xor(base, off, kL);
+        ent += __shfl_xor(ent, off, kL);
+      }
+      base *= a.baseline_cost;
+      ent *= a.entropy_cost;
+      if (s == 0 && lane_ok && a.lane_losses) {
+        a.lane_losses[3 * b + 0] = static_cast<float>(pg);
+        a.lane_losses[3 * b + 1] = static_cast<float>(base);
+        a.lane_losses[3 * b + 2] = static_cast<float>(ent);
+      }
+      if (s != 0 || !lane_ok) pg = base = ent = 0.0;
+      finish_losses<NT>(a, pg, base, ent, red_scratch);
     }
-    base *= a.baseline_cost;
-    ent *= a.entropy_cost;
-    if (s == 0 && lane_ok && a.lane_losses) {
-      a.lane_losses[3 * b + 0] = static_cast<float>(pg);
-      a.lane_losses[3 * b + 1] = static_cast<float>(base);
-      a.lane_losses[3 * b + 2] = static_cast<float>(ent);
-    }
-    if (s != 0 || !lane_ok) pg = base = ent = 0.0;
-    finish_losses<NT>(a, pg, base, ent, red_scratch);
   }
 }
 
+// Workgroups of the multi-tile kernel that fit on a compute unit at once,
+// asked of the runtime once (0 if it cannot say).
 template <int A_, int LANES, typename In, bool kGrad>
-void launch_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int64_t vec_tiles) {
+int multi_workgroups_per_cu() {
+  static std::atomic<int> cached{-1};
+  int n = cached.load(std::memory_order_relaxed);
+  if (n < 0) {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &blocks, reinterpret_cast<const void*>(tiled_kernel<A_, LANES, In, kGrad, false, true>),
+            LANES * kL, 0) != hipSuccess) {
+      (void)hipGetLastError();  // not a launch error: the single-tile kernel runs instead
+      blocks = 0;
+    }
+    n = blocks > 0 ? blocks : 0;
+    cached.store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Compute units of the current device (0 if the runtime cannot say).
+int compute_units() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cached[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Launches the kernel; returns its grid size.  The multi-tile kernel runs when
+// every tile is a vector tile, the tiles are a whole multiple (at least two) of
+// the resident workgroups, and the ratio takes the float32 mode.  Elsewhere one
+// workgroup per tile measured as fast or faster: a batch that is not a whole
+// multiple would leave some workgroups a tile short, and the float64 ratio
+// mode has no registers to spare for the longer walk.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise>
+int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
+                      bool allow_multi) {
+  if constexpr (!kPrecise) {
+    if (allow_multi && vec_tiles == tiles) {
+      const int64_t resident = static_cast<int64_t>(multi_workgroups_per_cu<A_, LANES, In, kGrad>()) *
+                               compute_units();
+      if (resident > 0 && tiles >= 2 * resident && tiles % resident == 0) {
+        hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, false, true>), dim3(static_cast<unsigned>(resident)),
+                           dim3(LANES * kL), 0, st, a, vec_tiles, tiles / resident);
+        return resident;
+      }
+    }
+  }
+  hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, kPrecise, false>), dim3(static_cast<unsigned>(tiles)),
+                     dim3(LANES * kL), 0, st, a, vec_tiles, int64_t(1));
+  return tiles;
+}
+
+template <int A_, int LANES, typename In, bool kGrad>
+int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
+                    bool allow_multi) {
   // float32 ratios suffice unless V-trace's weights can exceed 1 (products of c
   // can then grow and amplify rounding).  The other variants use the ratio, if
   // at all, only as one factor of one step's advantage.
   const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
-  if (precise)
-    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, true>), dim3(blocks), dim3(LANES * kL),
-                       0, st, a, vec_tiles);
-  else
-    hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, false>), dim3(blocks), dim3(LANES * kL),
-                       0, st, a, vec_tiles);
+  if (precise) return launch_kernel<A_, LANES, In, kGrad, true>(a, st, tiles, vec_tiles, allow_multi);
+  return launch_kernel<A_, LANES, In, kGrad, false>(a, st, tiles, vec_tiles, allow_multi);
 }
 
 template <int A_, int LANES, typename In>
-hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg) {
-  const int64_t blocks = (a.B + LANES - 1) / LANES;
-  *nwg = blocks;
+hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
+  const int64_t tiles = (a.B + LANES - 1) / LANES;
   // Vector path: full lane tiles whose time rows start on 16-byte boundaries.
   const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
   const int64_t out_row = a.B * A_ * (a.grad_bf16 ? 2 : 4);
   const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
   const int64_t vec_tiles = aligned ? a.B / LANES : 0;
   if (mode == Mode::LossGrad)
-    launch_mode<A_, LANES, In, true>(a, st, static_cast<unsigned>(blocks), vec_tiles);
+    *nwg = launch_mode<A_, LANES, In, true>(a, st, tiles, vec_tiles, allow_multi);
   else
-    launch_mode<A_, LANES, In, false>(a, st, static_cast<unsigned>(blocks), vec_tiles);
+    *nwg = launch_mode<A_, LANES, In, false>(a, st, tiles, vec_tiles, allow_multi);
   return hipGetLastError();
 }
 
@@ -406,13 +561,13 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A == 9 || a.A == 
 // CUs); A = 18 uses 16 lanes for fp32 logits (1152-byte runs, nine 128-byte
 // lines) and 32 for bf16 logits.
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
-                        int64_t* num_workgroups) {
+                        int64_t* num_workgroups, bool allow_multi) {
   if (lt == LogitsType::F32) {
-    if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups);
-    if (a.A == 9) return launch_shape<9, 16, float>(a, mode, st, num_workgroups);
+    if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups, allow_multi);
+    if (a.A == 9) return launch_shape<9, 16, float>(a, mode, st, num_workgroups, allow_multi);
   } else {
-    if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups);
-    if (a.A == 9) return launch_shape<9, 16, uint16_t>(a, mode, st, num_workgroups);
+    if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups, allow_multi);
+    if (a.A == 9) return launch_shape<9, 16, uint16_t>(a, mode, st, num_workgroups, allow_multi);
   }
   return hipErrorNotSupported;
 }

@@ -280,6 +280,52 @@ def test_kernels_agree(monkeypatch, pidx, kernel):
                          np_out(getattr(b, name)))
 
 
+def _bits(t):
+    return t.view(torch.int16 if t.element_size() == 2 else torch.int32).cpu().numpy()
+
+
+@pytest.mark.parametrize("A,bf16,grad", [(18, False, "float32"), (18, True, "float32"),
+                                         (9, False, "bfloat16"), (9, True, "float32")])
+def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
+    """A batch whose tile count is a whole multiple (at least two) of the
+    workgroups the chip holds at once runs the tiled kernel's multi-tile walk;
+    on a 256-CU part B = 24576 is one for every logit type and action count.
+    Every per-step and per-lane output must be bit-identical to the walk with
+    one workgroup per tile (the same arithmetic per lane; only the order of the
+    batch totals differs), the totals must agree within the sum tolerance, and
+    sampled lanes must match the oracle.  The targets-only call likewise."""
+    T, B = 40, 24576
+    tr = make_random(T, B, A, 77 + A, noise_std=1.0, end_prob=0.02, bf16=bf16)
+    dev = to_device(tr)
+    gd = torch.bfloat16 if grad == "bfloat16" else torch.float32
+    lanes = sorted(set([0, 1, 15, 16, 17, B // 3, B // 2, B - 17, B - 16, B - 1]
+                       + list(range(511, B, 4093))))
+    for p in (PARAM_SETS[4][0], PARAM_SETS[4][2]):
+        log_case(f"multi-tile walk T={T} B={B} A={A} bf16={bf16} grad={grad} {p.label()}")
+        monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+        a = run_loss_grad(dev, p, grad_dtype=gd)
+        ta = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+        b = run_loss_grad(dev, p, grad_dtype=gd)
+        tb = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
+        torch.cuda.synchronize()
+        monkeypatch.delenv("VTRACE_KERNEL")
+        for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses"):
+            x, y = getattr(a, name), getattr(b, name)
+            assert np.array_equal(_bits(x), _bits(y)), f"{name} differs between the two walks"
+        for x, y in zip(ta, tb):
+            assert np.array_equal(_bits(x), _bits(y)), "targets differ between the two walks"
+        assert_close("losses, multi vs single", np_out(a.losses), np_out(b.losses), rtol=1e-4,
+                     atol=1e-3)
+        lane = np_out(a.lane_losses).astype(np.float64)
+        assert_close("losses vs lane sums", np_out(a.losses)[1:].astype(np.float64),
+                     lane.sum(axis=0), rtol=1e-4, atol=1e-3)
+        if gd == torch.float32:
+            check_against_oracle(tr, p, a, lanes=lanes)
+    del dev
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
                                       (2, True)])
