@@ -502,18 +502,21 @@ int compute_units() {
 }
 
 // Launches the kernel; returns its grid size.  The multi-tile kernel runs when
-// every tile is a vector tile, the tiles are a whole multiple (at least two) of
-// the resident workgroups, and the ratio takes the float32 mode.  Elsewhere one
-// workgroup per tile measured as fast or faster: a batch that is not a whole
-// multiple would leave some workgroups a tile short, and the float64 ratio
-// mode has no registers to spare for the longer walk.
+// every tile is a vector tile, two or more of its workgroups fit on a CU, the
+// tiles are a whole multiple (at least two) of the resident workgroups, and the
+// ratio takes the float32 mode.  Elsewhere one workgroup per tile measured as
+// fast or faster: a batch that is not a whole multiple would leave some
+// workgroups a tile short, the float64 ratio mode has no registers to spare for
+// the longer walk, and with one resident workgroup per CU (the 512-thread
+// kernel of bfloat16 logits with A = 18) the multi-tile walk measured 4-10%
+// slower.
 template <int A_, int LANES, typename In, bool kGrad, bool kPrecise>
 int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                       bool allow_multi) {
   if constexpr (!kPrecise) {
-    if (allow_multi && vec_tiles == tiles) {
-      const int64_t resident = static_cast<int64_t>(multi_workgroups_per_cu<A_, LANES, In, kGrad>()) *
-                               compute_units();
+    const int per_cu = allow_multi && vec_tiles == tiles ? multi_workgroups_per_cu<A_, LANES, In, kGrad>() : 0;
+    if (per_cu >= 2) {
+      const int64_t resident = static_cast<int64_t>(per_cu) * compute_units();
       if (resident > 0 && tiles >= 2 * resident && tiles % resident == 0) {
         hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, false, true>), dim3(static_cast<unsigned>(resident)),
                            dim3(LANES * kL), 0, st, a, vec_tiles, tiles / resident);

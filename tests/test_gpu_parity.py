@@ -284,12 +284,13 @@ def _bits(t):
     return t.view(torch.int16 if t.element_size() == 2 else torch.int32).cpu().numpy()
 
 
-@pytest.mark.parametrize("A,bf16,grad", [(18, False, "float32"), (18, True, "float32"),
+@pytest.mark.parametrize("A,bf16,grad", [(18, False, "float32"), (18, False, "bfloat16"),
                                          (9, False, "bfloat16"), (9, True, "float32")])
 def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
     """A batch whose tile count is a whole multiple (at least two) of the
-    workgroups the chip holds at once runs the tiled kernel's multi-tile walk;
-    on a 256-CU part B = 24576 is one for every logit type and action count.
+    workgroups the chip holds at once runs the tiled kernel's multi-tile walk
+    (for the kernels that fit two or more workgroups per CU: all but bfloat16
+    logits with A = 18); on a 256-CU part B = 24576 is such a batch.
     Every per-step and per-lane output must be bit-identical to the walk with
     one workgroup per tile (the same arithmetic per lane; only the order of the
     batch totals differs), the totals must agree within the sum tolerance, and
