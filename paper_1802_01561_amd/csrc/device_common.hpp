@@ -119,10 +119,22 @@ __device__ __forceinline__ void block_sum3(double& x0, double& x1, double& x2, d
   }
 }
 
+// s_waitcnt immediate for vmcnt(0) alone (expcnt and lgkmcnt at their maxima).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 // Cross-workgroup loss reduction in the same launch.  Each workgroup stores its
 // three partial sums, then takes a ticket; the workgroup that draws the last
 // ticket adds all partials in workgroup order, writes `losses` and rearms the
 // counter for the next call.  Every thread of every workgroup must call this.
+//
+// Ordering without fences: the partials are written and read only with
+// device-scope atomic stores and loads, which the hardware performs where the
+// accesses of all XCDs meet (not in one XCD's L2).  A workgroup takes its
+// ticket only after its partial stores have completed (vmcnt(0)), so the
+// workgroup that draws the last ticket reads every partial.  A device-scope
+// fence would in addition write back and invalidate the XCD's L2 for ordinary
+// accesses, which nothing here needs; in a short call those fences cost
+// several microseconds.
 template <int kThreads>
 __device__ void finish_losses(const StepArgs& a, double pg, double base, double ent,
                               double* scratch) {
@@ -130,16 +142,17 @@ __device__ void finish_losses(const StepArgs& a, double pg, double base, double 
   block_sum3<kThreads>(pg, base, ent, scratch);
   if (threadIdx.x == 0) {
     double* p = a.partials + 3 * static_cast<size_t>(blockIdx.x);
-    p[0] = pg;
-    p[1] = base;
-    p[2] = ent;
-    __threadfence();  // release the partials before the ticket
-    const unsigned prev = atomicAdd(a.ticket, 1u);
+    __hip_atomic_store(p + 0, pg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 1, base, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 2, ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the compiler from moving them past the wait
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // the partial stores have completed
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    const unsigned prev = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == gridDim.x - 1);
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();  // acquire: every other workgroup's partials are visible
   double s0 = 0.0, s1 = 0.0, s2 = 0.0;
   for (unsigned i = threadIdx.x; i < gridDim.x; i += kThreads) {
     const double* p = a.partials + 3 * static_cast<size_t>(i);

@@ -124,8 +124,6 @@ __device__ __forceinline__ f32x4 mfma_k16(s16x4 a, s16x4 b, f32x4 c) {
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 constexpr int kRawBufferFlags = 0x00020000;  // raw buffer, 32-bit elements, no swizzle
 constexpr uint32_t kOutOfRange = 0xFFFFF000u;  // beyond every descriptor used here
-// s_waitcnt immediate for vmcnt(0) alone (expcnt and lgkmcnt at their maxima).
-constexpr int kWaitVmcnt0 = 0x0F70;
 
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes),
