@@ -121,7 +121,7 @@ def behaviour_log_probs(tr):
 
 
 def check_io_variant(tr, p, *, log_probs=False, reward_transform=None, grad_bf16=False,
-                     correction="vtrace", lanes=None):
+                     correction="vtrace", lanes=None, q_estimate="vtrace"):
     dev = to_device(tr)
     otr_args = list(oracle_args(tr))
     behaviour = "logits"
@@ -134,20 +134,20 @@ def check_io_variant(tr, p, *, log_probs=False, reward_transform=None, grad_bf16
     out = vt.vtrace_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
                               baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
                               with_vs=True, with_pg_advantages=True, with_lane_losses=True,
-                              correction=correction, behaviour=behaviour,
+                              correction=correction, q_estimate=q_estimate, behaviour=behaviour,
                               reward_transform=reward_transform, grad_dtype=gd)
     vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
-                               correction=correction, behaviour=behaviour,
+                               correction=correction, q_estimate=q_estimate, behaviour=behaviour,
                                reward_transform=reward_transform)
     torch.cuda.synchronize()
     if lanes is not None:
         idx = np.asarray(lanes)
         otr_args = [x[:, idx] if i != 6 else x[idx] for i, x in enumerate(otr_args)]
     o = oracle.loss_and_grads(*otr_args, p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
-                              p.entropy_cost, correction=correction, behaviour=behaviour,
-                              reward_transform=reward_transform)
+                              p.entropy_cost, correction=correction, q_estimate=q_estimate,
+                              behaviour=behaviour, reward_transform=reward_transform)
     pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
-    tag = f"lp={log_probs} r={reward_transform} bf16={grad_bf16} {correction}"
+    tag = f"lp={log_probs} r={reward_transform} bf16={grad_bf16} {correction}/{q_estimate}"
     assert_close(f"{tag} vs", pick(np_out(out.vs)), o.vs)
     assert_close(f"{tag} pg_advantages", pick(np_out(out.pg_advantages)), o.pg_advantages)
     assert_close(f"{tag} d_values", pick(np_out(out.d_values)), o.d_values)
@@ -197,3 +197,46 @@ def test_io_variants_stress_subset():
     for p in (Params(1.0, 1.0, 1.0), Params(math.inf, math.inf, 1.0)):
         log_case(f"stress, behaviour log-probabilities + bf16 grads, {p.label()}")
         check_io_variant(tr, p, log_probs=True, grad_bf16=True, lanes=STRESS_SUBSET)
+
+
+def _sweep_cases():
+    """Seeded random draws over every axis the entry points take."""
+    rng = np.random.default_rng(20261202)
+    cases = []
+    for _ in range(24):
+        cases.append(dict(
+            T=int(rng.choice([1, 5, 16, 17, 33, 64, 100, 130])),
+            B=int(rng.choice([1, 3, 16, 33, 64, 200, 512, 1000])),
+            A=int(rng.choice([9, 18, 9, 18, 5])),
+            bf16=bool(rng.random() < 0.3),
+            p=Params(float(rng.choice([1.0, 2.0, math.inf, 0.5])), float(rng.choice([1.0, 0.5, math.inf])),
+                     float(rng.choice([1.0, 0.95, 0.5]))),
+            correction=str(rng.choice(CORRECTIONS)), q_estimate=str(rng.choice(Q_ESTIMATES)),
+            log_probs=bool(rng.random() < 0.3), reward_transform=rng.choice([None, "clip", "asymmetric"]),
+            grad_bf16=bool(rng.random() < 0.3), lanes=None))
+    # whole multiples of the resident workgroups (multi-tile walk), on a lane subset
+    for A, bf16, lp, gb in [(18, False, False, False), (18, False, True, True), (9, False, False, True),
+                            (9, True, True, False)]:
+        cases.append(dict(T=20, B=24576, A=A, bf16=bf16, p=Params(1.0, 1.0, 1.0), correction="vtrace",
+                          q_estimate="vtrace", log_probs=lp, reward_transform="clip", grad_bf16=gb,
+                          lanes=[0, 1, 17, 4095, 12288, 24575]))
+    cases.append(dict(T=20, B=24576, A=18, bf16=False, p=Params(1.0, 0.5, 0.95), correction="one_step_is",
+                      q_estimate="baseline", log_probs=False, reward_transform=None, grad_bf16=False,
+                      lanes=[3, 777, 24560, 24575]))
+    return cases
+
+
+@pytest.mark.parametrize("i", range(len(_sweep_cases())))
+def test_random_sweep(i):
+    """Seeded draws mixing shapes (ragged T and B, A = 5, 9, 18), logit types,
+    corrections, Q estimates, behaviour log-probabilities, reward transforms,
+    bfloat16 gradients and clipping levels, each against the oracle; the last
+    cases are batches of 24576 lanes, whole multiples of the workgroups the
+    chip holds at once, which take the tiled kernel's multi-tile walk."""
+    c = _sweep_cases()[i]
+    tr = make_random(c["T"], c["B"], c["A"], 900 + i, noise_std=1.0, end_prob=0.03, bf16=c["bf16"])
+    tr.rewards = (tr.rewards * 2.5).astype(np.float32)  # exercise the clipping
+    log_case(f"sweep {i}: " + ", ".join(f"{k}={v}" for k, v in c.items() if k != "lanes"))
+    check_io_variant(tr, c["p"], log_probs=c["log_probs"], reward_transform=c["reward_transform"],
+                     grad_bf16=c["grad_bf16"], correction=c["correction"], q_estimate=c["q_estimate"],
+                     lanes=c["lanes"])
