@@ -163,6 +163,18 @@ def stored_traffic(avg_kernel_ms, path=COUNTERS_FILE, files=PLAIN_SOURCES):
     return nbytes / (avg_kernel_ms * 1e-3) / 1e9, nbytes
 
 
+def one_thread():
+    """Context in which NumPy's BLAS and OpenMP pools use one thread, so that the
+    oracle's timing is single-threaded whatever the host's defaults."""
+    from threadpoolctl import threadpool_limits
+    return threadpool_limits(limits=1)
+
+
+def host_info():
+    return {"cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
+            "host_cpus_available": len(os.sched_getaffinity(0)), "oracle_threads": 1}
+
+
 def cpu_baseline(tr, p, target_s):
     """The fp64 oracle, as it stands, on a bounded sample of lanes (all T), on one
     host thread.  Lanes are independent, so the sample is run in chunks of at
@@ -172,6 +184,10 @@ def cpu_baseline(tr, p, target_s):
     from synth import subset_lanes
 
     def run(n):
+        with one_thread():
+            return run_threads(n)
+
+    def run_threads(n):
         wall = 0.0
         for l0 in range(0, n, 2048):
             sub = subset_lanes(tr, np.arange(l0, min(n, l0 + 2048)))
@@ -198,8 +214,7 @@ def cpu_baseline(tr, p, target_s):
         "kind": "oracle",
         "sample": f"{n} of {tr.B} lanes x all T={tr.T} steps ({tr.T * n} steps) of the same "
                   f"batch, fp64 NumPy oracle, one thread, {wall:.1f} s wall",
-        "cpu_model": cpu_model(),
-        "host_cpus": os.cpu_count(),
+        **host_info(),
     }
 
 
@@ -261,11 +276,13 @@ def head_cpu_baseline(d, p, target_s, T, B):
         wall = 0.0
         for l0 in range(0, n, 256):
             hb = head_batch_from_device(d, list(range(l0, min(n, l0 + 256))))
-            t0 = time.perf_counter()
-            oracle.head_loss_and_grads(hb.hidden, hb.weight, hb.bias, hb.behaviour_logits,
-                                       hb.actions, hb.rewards, hb.discounts, hb.bootstrap_value,
-                                       p.rho_bar, p.c_bar, p.lam, p.baseline_cost, p.entropy_cost)
-            wall += time.perf_counter() - t0
+            with one_thread():
+                t0 = time.perf_counter()
+                oracle.head_loss_and_grads(hb.hidden, hb.weight, hb.bias, hb.behaviour_logits,
+                                           hb.actions, hb.rewards, hb.discounts,
+                                           hb.bootstrap_value, p.rho_bar, p.c_bar, p.lam,
+                                           p.baseline_cost, p.entropy_cost)
+                wall += time.perf_counter() - t0
         return wall
 
     n = 16
@@ -281,9 +298,9 @@ def head_cpu_baseline(d, p, target_s, T, B):
         "cores": 1,
         "kind": "oracle",
         "sample": f"{n} of {B} lanes x all T={T} steps ({T * n} steps) of the same batch, "
-                  f"fp64 NumPy oracle of the output layer + V-trace, {wall:.1f} s wall",
-        "cpu_model": cpu_model(),
-        "host_cpus": os.cpu_count(),
+                  f"fp64 NumPy oracle of the output layer + V-trace (BLAS on one thread), "
+                  f"{wall:.1f} s wall",
+        **host_info(),
     }
 
 

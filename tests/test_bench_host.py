@@ -62,3 +62,15 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cpu_baseline_runs_on_one_thread():
+    # the oracle's timing must be single-threaded (its BLAS calls included),
+    # and the JSON records the host it ran on
+    from threadpoolctl import threadpool_info
+    with bench.one_thread():
+        pools = threadpool_info()
+        assert all(p["num_threads"] == 1 for p in pools)
+    info = bench.host_info()
+    assert info["oracle_threads"] == 1 and info["host_cpus"] >= info["host_cpus_available"] >= 1
+    assert isinstance(info["cpu_model"], str)
