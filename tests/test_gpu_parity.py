@@ -327,6 +327,27 @@ def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("T", [1, 5, 16, 17, 33])
+def test_multi_tile_walk_unroll_lengths(T, monkeypatch):
+    """The multi-tile walk where a tile is one chunk (T <= 16: its carry reset
+    and its lane totals fall in the same iteration), exactly one chunk, and a
+    ragged second or third chunk: bit-identical to one workgroup per tile, and
+    sampled lanes against the oracle."""
+    B, A = 24576, 18
+    tr = make_random(T, B, A, 500 + T, noise_std=1.0, end_prob=0.05)
+    dev = to_device(tr)
+    p = PARAM_SETS[4][0]
+    log_case(f"multi-tile walk T={T} B={B} A={A}")
+    monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+    a = run_loss_grad(dev, p)
+    monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+    b = run_loss_grad(dev, p)
+    monkeypatch.delenv("VTRACE_KERNEL")
+    for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses"):
+        assert np.array_equal(_bits(getattr(a, name)), _bits(getattr(b, name))), name
+    check_against_oracle(tr, p, a, lanes=[0, 15, 16, 8191, 8192, B - 17, B - 1])
+
+
 @pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
                                       (2, True)])
