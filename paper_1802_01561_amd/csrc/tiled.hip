@@ -561,13 +561,22 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A == 9 || a.A == 
 
 // Lanes per workgroup: 16 (256 threads) for A = 9 keeps twice as many
 // workgroups in flight for mid-sized batches (a 4096-lane batch fills all 256
-// CUs); A = 18 uses 16 lanes for fp32 logits (1152-byte runs, nine 128-byte
-// lines) and 32 for bf16 logits.
+// CUs), but once 32-lane tiles cover every CU, fp32 A = 9 takes 32 (1152-byte
+// runs, nine 128-byte lines, as for fp32 A = 18): measured at T = 1000, 503 ->
+// 436 us for 16384 lanes and 2.00 -> 1.71 ms for 65536, while 4096 lanes
+// slow from 133 to 199 us (half the CUs idle).  bf16 A = 9 measured slower
+// with 32 lanes at every size and keeps 16.  A = 18 uses 16 lanes for fp32
+// logits and 32 for bf16 logits.
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups, bool allow_multi) {
   if (lt == LogitsType::F32) {
     if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups, allow_multi);
-    if (a.A == 9) return launch_shape<9, 16, float>(a, mode, st, num_workgroups, allow_multi);
+    if (a.A == 9) {
+      const int cus = compute_units();
+      if (cus > 0 && a.B >= 32 * static_cast<int64_t>(cus))
+        return launch_shape<9, 32, float>(a, mode, st, num_workgroups, allow_multi);
+      return launch_shape<9, 16, float>(a, mode, st, num_workgroups, allow_multi);
+    }
   } else {
     if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups, allow_multi);
     if (a.A == 9) return launch_shape<9, 16, uint16_t>(a, mode, st, num_workgroups, allow_multi);

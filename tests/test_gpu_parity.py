@@ -285,12 +285,14 @@ def _bits(t):
 
 
 @pytest.mark.parametrize("A,bf16,grad", [(18, False, "float32"), (18, False, "bfloat16"),
-                                         (9, False, "bfloat16"), (9, True, "float32")])
+                                         (9, True, "bfloat16"), (9, True, "float32")])
 def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
     """A batch whose tile count is a whole multiple (at least two) of the
     workgroups the chip holds at once runs the tiled kernel's multi-tile walk
-    (for the kernels that fit two or more workgroups per CU: all but bfloat16
-    logits with A = 18); on a 256-CU part B = 24576 is such a batch.
+    (for the kernels that fit two or more workgroups per CU: fp32 logits with
+    A = 18 and bf16 logits with A = 9; fp32 A = 9 takes 32-lane tiles at this
+    size and bf16 A = 18 fits one workgroup per CU); on a 256-CU part
+    B = 24576 is such a batch.
     Every per-step and per-lane output must be bit-identical to the walk with
     one workgroup per tile (the same arithmetic per lane; only the order of the
     batch totals differs), the totals must agree within the sum tolerance, and
@@ -323,6 +325,33 @@ def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
                      lane.sum(axis=0), rtol=1e-4, atol=1e-3)
         if gd == torch.float32:
             check_against_oracle(tr, p, a, lanes=lanes)
+    del dev
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,B", [(40, 8192), (33, 24576 + 32), (17, 65536)])
+def test_wide_tiles_for_nine_actions(T, B, monkeypatch):
+    """fp32 logits with A = 9 take 32-lane tiles once they cover every CU
+    (B >= 8192 on a 256-CU part): the same results as the generic lane-serial
+    kernel (tightly, weights <= 1) and, on sampled lanes, as the oracle."""
+    A = 9
+    tr = make_random(T, B, A, 700 + T, noise_std=1.0, end_prob=0.03)
+    dev = to_device(tr)
+    for p in (PARAM_SETS[4][0], PARAM_SETS[4][1]):
+        log_case(f"32-lane tiles T={T} B={B} A={A} {p.label()}")
+        monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+        a = run_loss_grad(dev, p)
+        check_against_oracle(tr, p, a, lanes=[0, 31, 32, B // 2, B - 33, B - 1])
+        if p is PARAM_SETS[4][0]:
+            monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
+            b = run_loss_grad(dev, p)
+            monkeypatch.delenv("VTRACE_KERNEL")
+            for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+                assert_close(f"32-lane vs lane_serial {name}", np_out(getattr(a, name)),
+                             np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
+            for name in ("lane_losses", "losses"):
+                assert_close(f"32-lane vs lane_serial {name}", np_out(getattr(a, name)),
+                             np_out(getattr(b, name)))
     del dev
     torch.cuda.empty_cache()
 
