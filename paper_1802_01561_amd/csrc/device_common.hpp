@@ -140,6 +140,17 @@ __device__ void finish_losses(const StepArgs& a, double pg, double base, double 
                               double* scratch) {
   __shared__ int s_last;
   block_sum3<kThreads>(pg, base, ent, scratch);
+  if (gridDim.x == 1) {
+    // One workgroup: its sums are the totals (the same values the ticket path
+    // would add to zero), without the round trips through memory.
+    if (threadIdx.x == 0) {
+      a.losses[0] = static_cast<float>(pg + base + ent);
+      a.losses[1] = static_cast<float>(pg);
+      a.losses[2] = static_cast<float>(base);
+      a.losses[3] = static_cast<float>(ent);
+    }
+    return;
+  }
   if (threadIdx.x == 0) {
     double* p = a.partials + 3 * static_cast<size_t>(blockIdx.x);
     __hip_atomic_store(p + 0, pg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
