@@ -691,8 +691,12 @@ __global__ __launch_bounds__(kFinishWaves* kWave) void head_finish_kernel(HeadAr
   else if (i < n_out)
     off = static_cast<size_t>(H) * C + static_cast<size_t>(i - n_w);
   double sum = 0.0;
-  if (i < n_out)
+  if (i < n_out) {
+    // Unrolled so that several rows' loads are in flight; the additions keep
+    // their order.
+#pragma unroll 8
     for (int k = wv; k < nwg; k += kFinishWaves) sum += static_cast<double>(a.grad_partials[k * stride + off]);
+  }
   s_q[wv][lane] = sum;
   __syncthreads();
   if (wv == 0 && i < n_out) {
@@ -703,17 +707,23 @@ __global__ __launch_bounds__(kFinishWaves* kWave) void head_finish_kernel(HeadAr
     else
       a.d_bias[i - n_w] = static_cast<float>(tot);
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0) {
+    // Loss totals: each thread adds the workgroups k = thread, thread + 1024,
+    // ..., then a fixed-order block reduction.
+    __shared__ double s_red[3 * kFinishWaves];
     double p0 = 0.0, p1 = 0.0, p2 = 0.0;
-    for (int k = 0; k < nwg; ++k) {
+    for (int k = threadIdx.x; k < nwg; k += kFinishWaves * kWave) {
       p0 += a.loss_partials[3 * k + 0];
       p1 += a.loss_partials[3 * k + 1];
       p2 += a.loss_partials[3 * k + 2];
     }
-    a.losses[0] = static_cast<float>(p0 + p1 + p2);
-    a.losses[1] = static_cast<float>(p0);
-    a.losses[2] = static_cast<float>(p1);
-    a.losses[3] = static_cast<float>(p2);
+    block_sum3<kFinishWaves * kWave>(p0, p1, p2, s_red);
+    if (threadIdx.x == 0) {
+      a.losses[0] = static_cast<float>(p0 + p1 + p2);
+      a.losses[1] = static_cast<float>(p0);
+      a.losses[2] = static_cast<float>(p1);
+      a.losses[3] = static_cast<float>(p2);
+    }
   }
 }
 
