@@ -35,7 +35,7 @@ METRIC = "trajectory steps/sec (T*B) for fused V-trace loss+grad; achieved HBM G
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "loss_grad_stress_counters.json")
 HEAD_COUNTERS_FILE = os.path.join(ROOT, "profiles", "head_stress_counters.json")
 # The sources each counted kernel is built from.
-PLAIN_SOURCES = ("tiled.hip", "row_stats.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
+PLAIN_SOURCES = ("tiled.hip", "tiled_impl.hpp", "row_stats.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
 HEAD_SOURCES = ("head.hip", "head.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
 
 

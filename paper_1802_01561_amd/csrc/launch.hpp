@@ -60,9 +60,18 @@ enum class Mode { Targets, LossGrad };
 hipError_t launch_lane_serial(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                               int64_t* num_workgroups);
 bool tiled_supported(const StepArgs& a, LogitsType lt);
-// allow_multi false keeps one workgroup per tile (no multi-tile walk).
+// The tiled kernel covers 2 <= A <= kTiledMaxActions (beyond, its per-thread
+// prefetch no longer fits the registers of two waves per SIMD).  allow_multi
+// false keeps one workgroup per tile (no multi-tile walk).
+constexpr int64_t kTiledMaxActions = 20;
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                         int64_t* num_workgroups, bool allow_multi);
+hipError_t launch_tiled_a2_8(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                             int64_t* num_workgroups, bool allow_multi);
+hipError_t launch_tiled_a10_14(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                               int64_t* num_workgroups, bool allow_multi);
+hipError_t launch_tiled_a15_20(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
+                               int64_t* num_workgroups, bool allow_multi);
 bool wide_supported(const StepArgs& a, LogitsType lt);
 hipError_t launch_wide(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                        int64_t* num_workgroups);

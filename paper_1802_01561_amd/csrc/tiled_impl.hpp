@@ -1,0 +1,572 @@
+// Tiled V-trace kernel, templated on the action count A (instantiated for
+// 2 <= A <= 20 by tiled.hip and tiled_a*.hip; A = 9 is DeepMind Lab's set,
+// A = 18 the full Atari set).
+//
+// Work split.  A tile is LANES consecutive lanes (batch entries) for the whole
+// unroll; a workgroup walks a tile's time backwards in chunks of L = 16 steps,
+// so every carry of the reverse recursion stays inside the workgroup.  Within
+// a chunk, thread (lane, s) handles step t = t0 + s; the 16 threads of one lane
+// are one DPP row of a wave.  When the batch has a whole multiple of the tiles
+// the chip holds workgroups at once, each resident workgroup walks an equal
+// share of tiles as one continuous sequence of chunks.
+//
+// Data path per chunk.
+//  1. For each t the chunk's logits are one contiguous run of LANES*A elements
+//     (1152 bytes for fp32 logits: nine 128-byte lines).  Threads copy both
+//     tensors' runs with 16-byte loads into LDS.  These whole-line logit loads
+//     and the gradient stores are used once, so they carry the non-temporal
+//     hint; the [T,B] scalars, whose 64-byte halves neighbouring workgroups
+//     share in L2, do not.  The loads of chunk k+1
+//     (and its per-step scalars) are issued before chunk k is computed and land
+//     in registers, so their latency hides behind the arithmetic.
+//  2. Each thread reads its own two rows from LDS: row maxima, exponent sums,
+//     the importance ratio (float64, see device_common.hpp), rho and c.
+//  3. The recursion v_t - V(x_t) = delta_t + gamma_t c_t (v_{t+1} - V(x_{t+1}))
+//     (Remark 1) is an affine map per step.  A suffix scan across the row (DPP
+//     row shifts) composes the chunk's maps; applying them to the carry from
+//     the later chunk gives every v_t of the chunk at once.
+//  4. Advantages, d_values and the gradient row follow.  Gradient rows go
+//     through LDS so that the global stores are whole 16-byte vectors along the
+//     contiguous [t, b0:b0+LANES, :] runs.
+//
+// Workgroups whose lane tile is full and whose rows are 16-byte aligned take
+// the vector path above; a ragged last tile (or unaligned rows) copies element
+// by element without prefetching.
+#pragma once
+
+#include <atomic>
+#include <type_traits>
+
+#include "device_common.hpp"
+#include "row_stats.hpp"
+#include "wave_ops.hpp"
+
+namespace vtrace {
+namespace {
+
+constexpr int kL = 16;  // steps per chunk = threads per lane row
+
+template <int A_, int LANES, typename In>
+struct Tile {
+  static constexpr int A = A_;
+  static constexpr int NT = LANES * kL;                        // threads per workgroup
+  static constexpr int SEG = LANES * A_;                       // elements per time row
+  static constexpr int IN_ROW16 = SEG * int(sizeof(In)) / 16;  // 16-byte vectors per row, logits
+  static constexpr int OUT_ROW16 = SEG * 4 / 16;               // 16-byte vectors per row, d_logits
+  // LDS rows are padded by one 16-byte vector: without it every step of a lane
+  // would read the same banks (a row is a multiple of 128 bytes).
+  static constexpr int IN_PITCH16 = IN_ROW16 + 1;
+  static constexpr int OUT_PITCH16 = OUT_ROW16 + 1;
+  static constexpr int IN_TILE16 = kL * IN_ROW16;    // vectors per tensor and chunk
+  static constexpr int OUT_TILE16 = kL * OUT_ROW16;
+  static constexpr int IN_LDS16 = kL * IN_PITCH16;   // LDS footprint per tensor
+  static constexpr int OUT_LDS16 = kL * OUT_PITCH16;
+  static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;  // vectors per thread, both tensors
+  static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;     // gradient vectors per thread
+  static constexpr int LDS16 = (2 * IN_LDS16 > OUT_LDS16) ? 2 * IN_LDS16 : OUT_LDS16;
+  static constexpr int IN_PITCH = IN_PITCH16 * 16 / int(sizeof(In));  // elements per LDS row
+  static constexpr int OUT_PITCH = OUT_PITCH16 * 4;                    // floats per LDS row
+  static_assert((SEG * int(sizeof(In))) % 16 == 0, "logit rows must be whole 16-byte vectors");
+  static_assert((SEG * 4) % 16 == 0, "gradient rows must be whole 16-byte vectors");
+  static_assert(NT % kWave == 0 && NT <= 1024, "bad workgroup size");
+  static_assert(OUT_ROW16 % 2 == 0, "bfloat16 gradient rows must be whole 16-byte vectors");
+};
+
+// Per-thread state carried along the chunk walk.
+struct Carry {
+  double V, v, A;  // V(x_{t+1}), v_{t+1}, v_{t+1} - V(x_{t+1}) at the later chunk's first step
+  double pg, base, ent;
+};
+
+
+// Walks one tile (kMulti false: `tile`, with the carry cy set up by the
+// caller), or (kMulti true, vector tiles only) the tiles first_tile + i *
+// tile_stride, i < ntiles, one after another as one loop over their chunks, so
+// that the prefetch runs across tile boundaries; each lane's loss totals are
+// then added to acc[3 * lane], a slot only the lane's step-0 thread touches.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kVec, bool kMulti>
+__device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t first_tile,
+                                           int64_t tile_stride, int64_t ntiles, Carry& cy,
+                                           double* acc) {
+  static_assert(kVec || !kMulti, "the multi-tile walk takes vector tiles only");
+  using S = Tile<A_, LANES, In>;
+  constexpr int NT = S::NT;
+  v4u* const lds_z = lds;
+  v4u* const lds_y = lds + S::IN_LDS16;
+
+  const int tid = threadIdx.x;
+  const int lane_local = tid / kL;
+  const int s = tid % kL;
+  const int64_t T = a.T, B = a.B;
+  const int nchunks = static_cast<int>((T + kL - 1) / kL);
+
+  // Byte stride of one time row of logits.
+  const int64_t in_row = B * A_ * int64_t(sizeof(In));
+  const bool beh_lp = a.behaviour_log_probs != 0;
+  // No-correction and epsilon-correction never look at the behaviour policy.
+  const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
+  const bool skip_y = beh_lp || no_ratio;
+  const bool grad_bf16 = a.grad_bf16 != 0;
+  const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
+  const int64_t out_row = B * A_ * gsz;
+  const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
+
+  // Register prefetch (vector path): NV 16-byte vectors covering both tensors,
+  // plus this thread's action, reward, discount and value, and at a tile's
+  // first chunk its lane's bootstrap value.
+  v4u pre[S::NV];
+  int32_t p_act = 0;
+  float p_r = 0.f, p_g = 0.f, p_V = 0.f, p_lmu = 0.f, p_boot = 0.f;
+
+  auto prefetch = [&](int64_t tile, int k) {
+    const int64_t b0 = tile * LANES;
+    const int64_t b = b0 + lane_local;
+    const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
+    const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
+    const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
+    const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+    const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row 0
+    static_for<S::NV>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      const int f = tid + i * NT;
+      const bool is_y = f >= S::IN_TILE16;
+      if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
+        const int g = is_y ? f - S::IN_TILE16 : f;
+        int r = g / S::IN_ROW16;
+        const int c = g % S::IN_ROW16;
+        r = r < neg ? neg : r;
+        const char* base = is_y ? yg : zg;
+        pre[i] = __builtin_nontemporal_load(
+            reinterpret_cast<const v4u*>(base + (t0 + r) * in_row + c * 16));
+      }
+    });
+    int64_t t = t0 + s;
+    t = t < 0 ? 0 : t;
+    if (lane_ok) {
+      const int64_t idx = t * B + b;
+      p_act = a.actions[idx];
+      p_r = a.rewards[idx];
+      p_g = a.discounts[idx];
+      p_V = a.values[idx];
+      if (beh_lp && !no_ratio) p_lmu = lmu_g[idx];
+      if (kMulti && k == 0) p_boot = a.bootstrap_value[b];
+    }
+  };
+
+  const double rho_bar = a.rho_bar, c_bar = a.c_bar, lam = a.lambda;
+  const float ce = a.entropy_cost;
+
+  int64_t tile = first_tile;  // advanced by the multi-tile walk only
+  int k = 0;
+  // Chunks to walk: a tile's, or all the tiles' (which may exceed 32 bits).
+  using Count = std::conditional_t<kMulti, int64_t, int>;
+  const Count total = kMulti ? static_cast<Count>(ntiles * nchunks) : static_cast<Count>(nchunks);
+  if constexpr (kVec) prefetch(tile, 0);
+  for (Count it = 0; it < total; ++it) {
+    const int64_t b0 = tile * LANES;
+    const int64_t b = b0 + lane_local;
+    const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
+    const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
+    char* const dg = static_cast<char*>(a.d_logits) + b0 * A_ * gsz;
+    if constexpr (kMulti) {
+      if (k == 0) {
+        // A new tile: the carry past its last step is the bootstrap value
+        // (v_T = V(x_T), so v_T - V(x_T) = 0).
+        cy.V = cy.v = p_boot;
+        cy.A = 0.0;
+      }
+    }
+    const int64_t t0 = T - static_cast<int64_t>(k + 1) * kL;
+    const int64_t t = t0 + s;
+    const bool step_ok = lane_ok && t >= 0;
+    const int64_t idx = t * B + b;
+
+    __syncthreads();  // the previous chunk is done with LDS
+    int32_t act;
+    float r32, g32, V32, lmu = 0.f;
+    if constexpr (kVec) {
+      static_for<S::NV>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        const int f = tid + i * NT;
+        const bool is_y = f >= S::IN_TILE16;
+        if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
+          const int g = is_y ? f - S::IN_TILE16 : f;
+          const int r = g / S::IN_ROW16, c = g % S::IN_ROW16;
+          lds[(is_y ? S::IN_LDS16 : 0) + r * S::IN_PITCH16 + c] = pre[i];
+        }
+      });
+      act = p_act;
+      r32 = p_r;
+      g32 = p_g;
+      V32 = p_V;
+      lmu = p_lmu;
+      __syncthreads();
+      if constexpr (kMulti) {
+        if (it + 1 < total) {
+          const bool next_tile = k + 1 == nchunks;
+          prefetch(next_tile ? tile + tile_stride : tile, next_tile ? 0 : k + 1);
+        }
+      } else {
+        if (k + 1 < nchunks) prefetch(tile, k + 1);
+      }
+    } else {
+      In* lz = reinterpret_cast<In*>(lds_z);
+      In* ly = reinterpret_cast<In*>(lds_y);
+      for (int e = tid; e < kL * S::SEG; e += NT) {
+        const int rr = e / S::SEG, c = e % S::SEG;
+        const int64_t te = t0 + rr;
+        if (te >= 0 && c < nb * A_) {
+          const int64_t off = (te * B + b0) * A_ + c;
+          lz[rr * S::IN_PITCH + c] = static_cast<const In*>(a.target_logits)[off];
+          if (!skip_y) ly[rr * S::IN_PITCH + c] = static_cast<const In*>(a.behaviour_logits)[off];
+        }
+      }
+      act = 0;
+      r32 = g32 = V32 = 0.f;
+      if (step_ok) {
+        act = a.actions[idx];
+        r32 = a.rewards[idx];
+        g32 = a.discounts[idx];
+        V32 = a.values[idx];
+        if (beh_lp && !no_ratio) lmu = lmu_g[idx];
+      }
+      __syncthreads();
+    }
+    r32 = transform_reward(r32, a.reward_transform);
+    if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
+
+    // This thread's rows.
+    const In* zr = reinterpret_cast<const In*>(lds_z) + s * S::IN_PITCH + lane_local * A_;
+    const In* yr = reinterpret_cast<const In*>(lds_y) + s * S::IN_PITCH + lane_local * A_;
+    const bool act_ok = act >= 0 && act < A_;
+    const int act_c = act_ok ? act : 0;
+    if (!act_ok) raise_error_flag(a.error_flag);
+    float e[A_];
+    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
+    const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
+                                          lam * clip_above(st.ratio, c_bar), lam, act_ok);
+
+    const double r = r32, g = g32, V = V32;
+    double V_next = dpp_f64<kRowShl1>(V);
+    if (s == kL - 1) V_next = cy.V;
+    const double delta = w.rho_v * (r + g * V_next - V);
+
+    // Suffix scan over the row.  Step 15 first absorbs the carry from the later
+    // chunk, so that after the scan D holds v_t - V(x_t) on every thread:
+    // (G, D) composes the maps of steps s..15 applied to that carry.
+    double G = g * w.c_v, D = delta;
+    if (s == kL - 1) D = fma(G, cy.A, D);
+    static_for<4>([&](auto I) {
+      constexpr int off = 1 << decltype(I)::value;
+      const double Gn = dpp_f64<0x100 + off>(G);
+      const double Dn = dpp_f64<0x100 + off>(D);
+      if (s + off < kL) {
+        D = fma(G, Dn, D);
+        G = G * Gn;
+      }
+    });
+    const double A_t = D;  // v_t - V(x_t)
+    const double v_t = V + A_t;
+    double v_next = dpp_f64<kRowShl1>(v_t);
+    if (s == kL - 1) v_next = cy.v;
+    const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+    const double adv = w.rho_pg * (r + g * q_next - V);
+
+    // The row's first step becomes the carry of the earlier chunk, held by the
+    // row's last thread, the only one that reads it.
+    cy.A = dpp_f64<kRowShr15>(A_t);
+    cy.v = dpp_f64<kRowShr15>(v_t);
+    cy.V = dpp_f64<kRowShr15>(V);
+
+    if (step_ok) {
+      if (a.vs) a.vs[idx] = static_cast<float>(v_t);
+      if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+    }
+
+    if constexpr (kGrad) {
+      // d_logits_j = adv (pi_j - 1[j=a]) + ce pi_j (log pi_j + H), where
+      // log pi_j + H = z_j - K.  For j != a this is e_j (alpha + beta z_j).
+      const float K = st.mz + st.log_s - st.H;
+      // epsilon-correction: the policy-gradient term is -adv log(pi_a + eps),
+      // whose gradient is adv pi_a/(pi_a + eps) (pi_j - 1[j=a]).
+      const float pa = st.e_a * st.inv_s;
+      const bool eps_mode = a.correction == kCorrEpsilon;
+      const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
+      const float adv32 = static_cast<float>(adv) * pg_w;
+      const float beta = st.inv_s * ce;
+      const float alpha = st.inv_s * adv32 - beta * K;
+      const float za = logit_to_float(zr[act_c]);
+      const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
+      if (step_ok) {
+        a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+        const double log_pa =
+            !act_ok ? NAN
+            : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
+                       : static_cast<double>(za - st.mz) - static_cast<double>(st.log_s);
+        cy.pg += -adv * log_pa;
+        cy.base += 0.5 * A_t * A_t;
+        cy.ent += -static_cast<double>(st.H);
+      }
+      float out[A_];
+#pragma unroll
+      for (int j = 0; j < A_; ++j) out[j] = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
+      __syncthreads();  // every row has been read: LDS now takes the gradient tile
+      float* lo = reinterpret_cast<float*>(lds) + s * S::OUT_PITCH + lane_local * A_;
+#pragma unroll
+      for (int j = 0; j < A_; ++j) lo[j] = out[j];
+      lo[act_c] = act_ok ? out_a : NAN;
+      __syncthreads();
+      if constexpr (kVec) {
+        const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
+        if (!grad_bf16) {
+          static_for<S::NO>([&](auto I) {
+            constexpr int i = decltype(I)::value;
+            const int f = tid + i * NT;
+            if (i * NT + NT <= S::OUT_TILE16 || f < S::OUT_TILE16) {
+              const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
+              if (rr >= neg)
+                __builtin_nontemporal_store(
+                    lds[rr * S::OUT_PITCH16 + cc],
+                    reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+            }
+          });
+        } else {
+          // bfloat16 rows: each 16-byte store packs two 16-byte LDS vectors.
+          constexpr int kRow16 = S::OUT_ROW16 / 2, kTile16 = S::OUT_TILE16 / 2;
+          for (int f = tid; f < kTile16; f += NT) {
+            const int rr = f / kRow16, cc = f % kRow16;
+            if (rr >= neg) {
+              const v4u lo = lds[rr * S::OUT_PITCH16 + 2 * cc];
+              const v4u hi = lds[rr * S::OUT_PITCH16 + 2 * cc + 1];
+              v4u pk;
+              pk.x = pack_bf16x2(__uint_as_float(lo.x), __uint_as_float(lo.y));
+              pk.y = pack_bf16x2(__uint_as_float(lo.z), __uint_as_float(lo.w));
+              pk.z = pack_bf16x2(__uint_as_float(hi.x), __uint_as_float(hi.y));
+              pk.w = pack_bf16x2(__uint_as_float(hi.z), __uint_as_float(hi.w));
+              __builtin_nontemporal_store(pk,
+                                          reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+            }
+          }
+        }
+      } else {
+        const float* lf = reinterpret_cast<const float*>(lds);
+        for (int e2 = tid; e2 < kL * S::SEG; e2 += NT) {
+          const int rr = e2 / S::SEG, cc = e2 % S::SEG;
+          const int64_t te = t0 + rr;
+          if (te >= 0 && cc < nb * A_) {
+            const float x = lf[rr * S::OUT_PITCH + cc];
+            const int64_t o = (te * B + b0) * A_ + cc;
+            if (grad_bf16)
+              static_cast<uint16_t*>(a.d_logits)[o] = to_bf16(x);
+            else
+              static_cast<float*>(a.d_logits)[o] = x;
+          }
+        }
+      }
+      if (kMulti && k == nchunks - 1) {
+        // The tile's last chunk: this lane's totals over the row (fixed
+        // butterfly order), then the workgroup's running sums.
+        double lp = cy.pg, lb = cy.base, le = cy.ent;
+#pragma unroll
+        for (int off = kL / 2; off > 0; off >>= 1) {
+          lp += __shfl_xor(lp, off, kL);
+          lb += __shfl_xor(lb, off, kL);
+          le += __shfl_xor(le, off, kL);
+        }
+        lb *= a.baseline_cost;
+        le *= a.entropy_cost;
+        if (s == 0 && lane_ok) {
+          if (a.lane_losses) {
+            a.lane_losses[3 * b + 0] = static_cast<float>(lp);
+            a.lane_losses[3 * b + 1] = static_cast<float>(lb);
+            a.lane_losses[3 * b + 2] = static_cast<float>(le);
+          }
+          acc[3 * lane_local + 0] += lp;
+          acc[3 * lane_local + 1] += lb;
+          acc[3 * lane_local + 2] += le;
+        }
+        cy.pg = cy.base = cy.ent = 0.0;
+      }
+    }
+    if (++k == nchunks && kMulti) {
+      k = 0;
+      tile += tile_stride;
+    }
+  }
+}
+
+// kMulti false: one workgroup per tile, tile xcd_tile(blockIdx), which puts
+// workgroups that run side by side on one XCD on neighbouring tiles, whose
+// [T,B] scalars share 128-byte lines in that XCD's L2.
+//
+// kMulti true: the grid is exactly the workgroups the chip holds at once and
+// each walks tiles_per_wg vector tiles, xcd_tile(blockIdx) + i * gridDim.x.
+// When a batch has a whole multiple of that many tiles, this runs it as one
+// even generation: one workgroup per tile would instead start a second wave of
+// workgroups whenever a slot frees, and leave the chip partly idle at the end.
+// The fp64 ratio mode with A > 18 is asked for two waves per SIMD explicitly:
+// left to itself the compiler gives A = 19 two registers more than fit.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise, bool kMulti>
+__global__ __launch_bounds__(LANES* kL, (kPrecise && A_ > 18) ? 2 : 1) void tiled_kernel(
+    StepArgs a, int64_t num_vec_tiles, int64_t tiles_per_wg) {
+  using S = Tile<A_, LANES, In>;
+  constexpr int NT = S::NT;
+  __shared__ v4u lds[S::LDS16];
+  __shared__ double red_scratch[3 * (NT / kWave)];
+
+  const int lane_local = threadIdx.x / kL;
+  const int s = threadIdx.x % kL;
+
+  if constexpr (kMulti) {
+    __shared__ double acc[3 * LANES];  // per-lane loss sums over the workgroup's tiles
+    if (s == 0) acc[3 * lane_local + 0] = acc[3 * lane_local + 1] = acc[3 * lane_local + 2] = 0.0;
+    Carry cy{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+    chunk_walk<A_, LANES, In, kGrad, kPrecise, true, true>(a, lds, xcd_tile(blockIdx.x, gridDim.x),
+                                                           gridDim.x, tiles_per_wg, cy, acc);
+    if constexpr (kGrad) {
+      double pg = 0.0, base = 0.0, ent = 0.0;
+      if (s == 0) {
+        pg = acc[3 * lane_local + 0];
+        base = acc[3 * lane_local + 1];
+        ent = acc[3 * lane_local + 2];
+      }
+      finish_losses<NT>(a, pg, base, ent, red_scratch);
+    }
+  } else {
+    const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int64_t b = tile * LANES + lane_local;
+    const bool lane_ok = b < a.B;
+    const double boot = lane_ok ? static_cast<double>(a.bootstrap_value[b]) : 0.0;
+    Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
+
+    if (tile < num_vec_tiles)
+      chunk_walk<A_, LANES, In, kGrad, kPrecise, true, false>(a, lds, tile, 0, 1, cy, nullptr);
+    else
+      chunk_walk<A_, LANES, In, kGrad, kPrecise, false, false>(a, lds, tile, 0, 1, cy, nullptr);
+
+    if constexpr (kGrad) {
+      // Per-lane totals over the row (fixed butterfly order), then the workgroup.
+      double pg = cy.pg, base = cy.base, ent = cy.ent;
+#pragma unroll
+      for (int off = kL / 2; off > 0; off >>= 1) {
+        pg += __shfl_xor(pg, off, kL);
+        base += __shfl_xor(base, off, kL);
+        ent += __shfl_xor(ent, off, kL);
+      }
+      base *= a.baseline_cost;
+      ent *= a.entropy_cost;
+      if (s == 0 && lane_ok && a.lane_losses) {
+        a.lane_losses[3 * b + 0] = static_cast<float>(pg);
+        a.lane_losses[3 * b + 1] = static_cast<float>(base);
+        a.lane_losses[3 * b + 2] = static_cast<float>(ent);
+      }
+      if (s != 0 || !lane_ok) pg = base = ent = 0.0;
+      finish_losses<NT>(a, pg, base, ent, red_scratch);
+    }
+  }
+}
+
+// Workgroups of the multi-tile kernel that fit on a compute unit at once,
+// asked of the runtime once (0 if it cannot say).
+template <int A_, int LANES, typename In, bool kGrad>
+int multi_workgroups_per_cu() {
+  static std::atomic<int> cached{-1};
+  int n = cached.load(std::memory_order_relaxed);
+  if (n < 0) {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &blocks, reinterpret_cast<const void*>(tiled_kernel<A_, LANES, In, kGrad, false, true>),
+            LANES * kL, 0) != hipSuccess) {
+      (void)hipGetLastError();  // not a launch error: the single-tile kernel runs instead
+      blocks = 0;
+    }
+    n = blocks > 0 ? blocks : 0;
+    cached.store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Compute units of the current device (0 if the runtime cannot say).
+int compute_units() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cached[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Launches the kernel; returns its grid size.  The multi-tile kernel runs when
+// every tile is a vector tile, two or more of its workgroups fit on a CU, the
+// tiles are a whole multiple (at least two) of the resident workgroups, and the
+// ratio takes the float32 mode.  Elsewhere one workgroup per tile measured as
+// fast or faster: a batch that is not a whole multiple would leave some
+// workgroups a tile short, the float64 ratio mode has no registers to spare for
+// the longer walk, and with one resident workgroup per CU (the 512-thread
+// kernel of bfloat16 logits with A = 18) the multi-tile walk measured 4-10%
+// slower.
+template <int A_, int LANES, typename In, bool kGrad, bool kPrecise>
+int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
+                      bool allow_multi) {
+  if constexpr (!kPrecise) {
+    const int per_cu = allow_multi && vec_tiles == tiles ? multi_workgroups_per_cu<A_, LANES, In, kGrad>() : 0;
+    if (per_cu >= 2) {
+      const int64_t resident = static_cast<int64_t>(per_cu) * compute_units();
+      if (resident > 0 && tiles >= 2 * resident && tiles % resident == 0) {
+        hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, false, true>), dim3(static_cast<unsigned>(resident)),
+                           dim3(LANES * kL), 0, st, a, vec_tiles, tiles / resident);
+        return resident;
+      }
+    }
+  }
+  hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, kGrad, kPrecise, false>), dim3(static_cast<unsigned>(tiles)),
+                     dim3(LANES * kL), 0, st, a, vec_tiles, int64_t(1));
+  return tiles;
+}
+
+template <int A_, int LANES, typename In, bool kGrad>
+int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
+                    bool allow_multi) {
+  // float32 ratios suffice unless V-trace's weights can exceed 1 (products of c
+  // can then grow and amplify rounding).  The other variants use the ratio, if
+  // at all, only as one factor of one step's advantage.
+  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+  if (precise) return launch_kernel<A_, LANES, In, kGrad, true>(a, st, tiles, vec_tiles, allow_multi);
+  return launch_kernel<A_, LANES, In, kGrad, false>(a, st, tiles, vec_tiles, allow_multi);
+}
+
+template <int A_, int LANES, typename In>
+hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
+  const int64_t tiles = (a.B + LANES - 1) / LANES;
+  // Vector path: full lane tiles whose time rows start on 16-byte boundaries.
+  const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
+  const int64_t out_row = a.B * A_ * (a.grad_bf16 ? 2 : 4);
+  const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
+  const int64_t vec_tiles = aligned ? a.B / LANES : 0;
+  if (mode == Mode::LossGrad)
+    *nwg = launch_mode<A_, LANES, In, true>(a, st, tiles, vec_tiles, allow_multi);
+  else
+    *nwg = launch_mode<A_, LANES, In, false>(a, st, tiles, vec_tiles, allow_multi);
+  return hipGetLastError();
+}
+
+// Launch for action count A with 16 lanes per workgroup, fp32 or bf16 logits.
+template <int A_>
+hipError_t launch_shape_16(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st, int64_t* nwg,
+                           bool allow_multi) {
+  if (lt == LogitsType::F32) return launch_shape<A_, 16, float>(a, mode, st, nwg, allow_multi);
+  return launch_shape<A_, 16, uint16_t>(a, mode, st, nwg, allow_multi);
+}
+
+}  // namespace
+}  // namespace vtrace

@@ -329,6 +329,40 @@ def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
     torch.cuda.empty_cache()
 
 
+OTHER_ACTION_COUNTS = [2, 3, 4, 5, 6, 7, 8, 10, 11, 12, 13, 14, 15, 16, 17, 19, 20]
+
+
+@pytest.mark.parametrize("A", OTHER_ACTION_COUNTS)
+def test_tiled_other_action_counts(A, monkeypatch):
+    """Every action count 2 <= A <= 20 takes the tiled kernel: ragged shapes
+    against the oracle (fp32 and bf16 logits, weights clipped at 1 and
+    unclipped), and a 16384-lane batch (which takes the multi-tile walk where
+    it fits) against the generic lane-serial kernel and, on sampled lanes, the
+    oracle."""
+    for bf16 in (False, True):
+        tr = make_random(37, 45, A, 1100 + A, noise_std=1.0, end_prob=0.05, bf16=bf16)
+        for p in (PARAM_SETS[4][0], PARAM_SETS[4][1]):
+            log_case(f"tiled A={A} T=37 B=45 bf16={bf16} {p.label()}")
+            check_against_oracle(tr, p, run_loss_grad(to_device(tr), p))
+    T, B = 20, 16384
+    tr = make_random(T, B, A, 1200 + A, noise_std=1.0, end_prob=0.03)
+    dev = to_device(tr)
+    p = PARAM_SETS[4][0]
+    log_case(f"tiled A={A} T={T} B={B} against lane_serial")
+    monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+    a = run_loss_grad(dev, p)
+    check_against_oracle(tr, p, a, lanes=[0, 15, 16, B // 2, B - 1])
+    monkeypatch.setenv("VTRACE_KERNEL", "lane_serial")
+    b = run_loss_grad(dev, p)
+    monkeypatch.delenv("VTRACE_KERNEL")
+    for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+        assert_close(f"A={A} tiled vs lane_serial {name}", np_out(getattr(a, name)),
+                     np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
+    for name in ("lane_losses", "losses"):
+        assert_close(f"A={A} tiled vs lane_serial {name}", np_out(getattr(a, name)),
+                     np_out(getattr(b, name)))
+
+
 @pytest.mark.parametrize("T,B", [(40, 8192), (33, 24576 + 32), (17, 65536)])
 def test_wide_tiles_for_nine_actions(T, B, monkeypatch):
     """fp32 logits with A = 9 take 32-lane tiles once they cover every CU
