@@ -13,8 +13,13 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A >= 2 && a.A <= 
 // runs, nine 128-byte lines, as for fp32 A = 18): measured at T = 1000, 503 ->
 // 436 us for 16384 lanes and 2.00 -> 1.71 ms for 65536, while 4096 lanes
 // slow from 133 to 199 us (half the CUs idle).  bf16 A = 9 measured slower
-// with 32 lanes at every size and keeps 16.  A = 18 uses 16 lanes for fp32
-// logits and 32 for bf16 logits.
+// with 32 lanes at every size and keeps 16.  fp32 A = 18 uses 16 lanes (its
+// rows are already 1152 bytes).  bf16 A = 18 is the mirror image of fp32
+// A = 9: 32 lanes (1152-byte rows) once the tiles fill every CU twice, 16
+// below that (T = 1000: 4096 lanes 252 -> 167 us and 8192 lanes 297 -> 275 us
+// with 16; 16384 lanes 593 -> 558 us and 32768 lanes 1.23 -> 1.10 ms with 32),
+// and 32 when the whole batch is one tile (one workgroup, whose loss sums need
+// no cross-workgroup reduction).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups, bool allow_multi) {
   if (lt == LogitsType::F32) {
@@ -26,7 +31,12 @@ hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t
       return launch_shape<9, 16, float>(a, mode, st, num_workgroups, allow_multi);
     }
   } else {
-    if (a.A == 18) return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups, allow_multi);
+    if (a.A == 18) {
+      const int cus = compute_units();
+      if (a.B <= 32 || (cus > 0 && a.B >= 64 * static_cast<int64_t>(cus)))
+        return launch_shape<18, 32, uint16_t>(a, mode, st, num_workgroups, allow_multi);
+      return launch_shape<18, 16, uint16_t>(a, mode, st, num_workgroups, allow_multi);
+    }
     if (a.A == 9) return launch_shape<9, 16, uint16_t>(a, mode, st, num_workgroups, allow_multi);
   }
   // The other action counts, 16 lanes per workgroup (instantiated in three

@@ -261,7 +261,8 @@ def test_kernels_agree(monkeypatch, pidx, kernel):
     unclipped."""
     p = PARAM_SETS[4][pidx]
     tight = pidx == 0
-    for (T, B, A, bf16) in [(100, 4096, 9, False), (60, 1000, 18, False), (50, 777, 9, True)]:
+    for (T, B, A, bf16) in [(100, 4096, 9, False), (60, 1000, 18, False), (50, 777, 9, True),
+                            (40, 1000, 18, True), (20, 32, 18, True)]:
         tr = make_random(T, B, A, 31 + A, noise_std=1.0, bf16=bf16)
         dev = to_device(tr)
         log_case(f"kernel agreement {kernel} T={T} B={B} A={A} bf16={bf16} {p.label()}")
