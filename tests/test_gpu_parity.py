@@ -186,7 +186,7 @@ def test_deterministic_and_workspace_reuse():
     dev = to_device(tr)
     ws = vt.Workspace(tr.T, tr.B, tr.A)
     p = PARAM_SETS[3][0]
-    log_case("determinism, config 3")
+    log_case("determinism, 30-task batch T=100 B=4096 A=9")
     a = run_loss_grad(dev, p, workspace=ws)
     b = run_loss_grad(dev, p, workspace=ws)
     for x, y in zip(a, b):
