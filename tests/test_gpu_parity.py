@@ -193,6 +193,34 @@ def test_deterministic_and_workspace_reuse():
         assert np_out(x).tobytes() == np_out(y).tobytes()
 
 
+@pytest.mark.parametrize("T,B,A", [(16, 4096, 9), (100, 4096, 9), (20, 24576, 18)])
+def test_loss_reduction_across_back_to_back_calls(T, B, A):
+    """The cross-workgroup loss reduction publishes each workgroup's partial
+    before its ticket; a partial read before it landed would still hold the
+    previous call's value.  Two different batches of the same shape alternate
+    on one workspace, 200 calls back to back on one stream, each writing its
+    own losses buffer: every call must reproduce its batch's losses bit for
+    bit."""
+    trs = [make_random(T, B, A, 4000 + k, noise_std=1.0, end_prob=0.03) for k in range(2)]
+    devs = [to_device(tr) for tr in trs]
+    p = PARAM_SETS[4][0]
+    ws = vt.Workspace(T, B, A)
+    log_case(f"back-to-back loss reductions T={T} B={B} A={A}")
+    ref = [np_out(run_loss_grad(d, p, workspace=ws).losses) for d in devs]
+    assert not np.array_equal(ref[0], ref[1])
+    first = run_loss_grad(devs[0], p, workspace=ws)
+    n = 200
+    losses = [torch.empty(4, dtype=torch.float32, device="cuda") for _ in range(n)]
+    for i in range(n):
+        out = first._replace(losses=losses[i])
+        vt.vtrace_loss_grad(**devs[i % 2], rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                            baseline_cost=p.baseline_cost, entropy_cost=p.entropy_cost,
+                            workspace=ws, out=out)
+    torch.cuda.synchronize()
+    for i in range(n):
+        assert np_out(losses[i]).tobytes() == ref[i % 2].tobytes(), f"call {i}"
+
+
 def test_lane_permutation_is_bit_exact():
     tr = make_random(50, 96, 9, 8)
     perm = np.random.default_rng(0).permutation(96)
