@@ -221,6 +221,43 @@ def test_loss_reduction_across_back_to_back_calls(T, B, A):
         assert np_out(losses[i]).tobytes() == ref[i % 2].tobytes(), f"call {i}"
 
 
+@pytest.mark.parametrize("T,B,A", [(100, 32, 9), (100, 4096, 9), (20, 16384, 18)])
+def test_graph_capture_replays(T, B, A):
+    """The call captured in a HIP graph (the time-parallel, tiled and
+    multi-tile kernels by shape) and replayed several times, with eager calls
+    on other inputs and synchronisations in between: every replay must equal
+    the eager result bit for bit (the loss ticket rearms itself; nothing in
+    the call is a memset)."""
+    trs = [make_random(T, B, A, 5000 + k, noise_std=1.0, end_prob=0.03) for k in range(2)]
+    devs = [to_device(tr) for tr in trs]
+    p = PARAM_SETS[4][0]
+    ws = vt.Workspace(T, B, A)
+    log_case(f"graph capture T={T} B={B} A={A}")
+    eager = run_loss_grad(devs[0], p, workspace=ws)
+    ref = {k: np_out(getattr(eager, k)).tobytes() for k in ("losses", "d_logits", "d_values", "vs")}
+    out = vt.vtrace_loss_grad(**devs[0], rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                              with_vs=True, with_pg_advantages=True, with_lane_losses=True,
+                              workspace=ws)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            vt.vtrace_loss_grad(**devs[0], rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                                workspace=ws, out=out)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for k in ("losses", "d_logits", "d_values", "vs"):
+            getattr(out, k).fill_(-1.0)
+        g.replay()
+        torch.cuda.synchronize()
+        for k in ("losses", "d_logits", "d_values", "vs"):
+            assert np_out(getattr(out, k)).tobytes() == ref[k], f"replay {rep}: {k}"
+        other = run_loss_grad(devs[1], p, workspace=ws)  # eager work between replays
+        assert not np.array_equal(np_out(other.losses), np_out(eager.losses))
+
+
 def test_lane_permutation_is_bit_exact():
     tr = make_random(50, 96, 9, 8)
     perm = np.random.default_rng(0).permutation(96)
