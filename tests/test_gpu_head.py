@@ -8,10 +8,9 @@ losses over a lane's steps, the loss totals over all steps, and each d_hidden
 element over the A + 1 output columns.  An error of up to 1e-4 of each term
 (the per-element bound) adds up, for independent errors, to about 1e-4 times
 the root-sum-square of the terms, so sums use
-|g - o| <= 1e-5 + 1e-4 |o| + 1e-4 RSS.  Unlike the plain loss, whose logits are
-exact inputs, the layer's logits carry float32 rounding, and a loss sum with
-heavy cancellation (terms adding to 10^4 times the result) can exceed the plain
-bound.  bfloat16 d_hidden adds its rounding (2^-8 relative).
+|g - o| <= 1e-5 + 1e-4 |o| + 1e-4 RSS, as the plain loss's sums do; here the
+layer's float32 logits add their own rounding to every term.  bfloat16
+d_hidden adds its rounding (2^-8 relative).
 """
 
 import math
@@ -22,7 +21,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import ATOL, RTOL, assert_close, log_case, np_out, require_gpu
+from gpu_util import ATOL, RTOL, assert_close, assert_sum_close, log_case, np_out, require_gpu
 from synth import HEAD_CONFIGS, Params, make_head, make_head_config, subset_head_lanes
 
 pytestmark = pytest.mark.gpu
@@ -52,18 +51,6 @@ def head_to_device(hb, behaviour=None, behaviour_bf16=False):
                 head_bias=d(hb.bias), behaviour_logits=beh, actions=d(hb.actions),
                 rewards=d(hb.rewards), discounts=d(hb.discounts),
                 bootstrap_value=d(hb.bootstrap_value))
-
-
-def assert_sum_close(name, got, expect, rss):
-    got = np.asarray(got, dtype=np.float64)
-    err = np.abs(got - expect)
-    bound = ATOL + RTOL * np.abs(expect) + RTOL * rss
-    bad = ~(err <= bound)
-    if bad.any():
-        ratio = np.where(np.isfinite(err), err / bound, np.inf)
-        worst = np.unravel_index(np.argmax(ratio), ratio.shape)
-        raise AssertionError(f"{name}: {int(bad.sum())} of {bad.size} outside the sum bound; worst at "
-                             f"{worst}: got {got[worst]!r} expected {expect[worst]!r} rss {rss[worst]!r}")
 
 
 def run_head(dev, p, **kw):

@@ -12,7 +12,8 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from gpu_util import (assert_close, assert_sum_close, log_case, loss_term_rss, np_out, oracle_args,
+                      require_gpu, to_device)
 from synth import PARAM_SETS, make_config, make_random, subset_lanes
 from synth.trajectories import STRESS_SUBSET
 
@@ -39,9 +40,10 @@ def check_against_oracle(tr, p, out, lanes=None):
     assert_close("d_values", pick(np_out(out.d_values)), o.d_values)
     assert_close("d_logits", pick(np_out(out.d_logits)), o.d_logits)
     lane = np_out(out.lane_losses)
-    assert_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses)
+    rss_lane, rss_tot = loss_term_rss(o)
+    assert_sum_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses, rss_lane)
     if lanes is None:
-        assert_close("losses", np_out(out.losses), o.losses)
+        assert_sum_close("losses", np_out(out.losses), o.losses, rss_tot)
     return o
 
 
@@ -92,6 +94,33 @@ def test_stress_subset_matches_oracle(stress, pidx):
     losses = np_out(out.losses).astype(np.float64)
     assert_close("losses vs lane sums", losses[1:], lane.sum(axis=0), rtol=1e-4, atol=1e-3)
     assert losses[0] == pytest.approx(losses[1:].sum(), rel=1e-6)
+
+
+def test_stress_every_lane_matches_oracle(stress):
+    """The full stress launch (T=1000, B=16384, A=18; the multi-tile walk) with
+    (1, 1, 1), every output element against the oracle, which runs on 2048
+    lanes at a time to bound host memory (lane losses and totals with the sum
+    bound); the totals against the fp64 sum of the oracle's lane losses."""
+    tr, dev = stress
+    p = PARAM_SETS[4][0]
+    log_case("stress T=1000 B=16384 A=18, every lane against the oracle")
+    out = run_loss_grad(dev, p)
+    got = {k: np_out(getattr(out, k)) for k in ("vs", "pg_advantages", "d_values", "d_logits")}
+    lane = np_out(out.lane_losses)
+    o_lane, s2 = [], np.zeros(3)
+    for l0 in range(0, tr.B, 2048):
+        lanes = list(range(l0, min(tr.B, l0 + 2048)))
+        o = oracle.loss_and_grads(*oracle_args(subset_lanes(tr, lanes)), p.rho_bar, p.c_bar, p.lam,
+                                  p.baseline_cost, p.entropy_cost)
+        for k, ov in (("vs", o.vs), ("pg_advantages", o.pg_advantages), ("d_values", o.d_values),
+                      ("d_logits", o.d_logits)):
+            assert_close(f"{k} lanes {l0}..", got[k][:, l0:l0 + len(lanes)], ov)
+        rss_lane, _ = loss_term_rss(o)
+        assert_sum_close(f"lane_losses {l0}..", lane[l0:l0 + len(lanes)], o.lane_losses, rss_lane)
+        o_lane.append(o.lane_losses.astype(np.float64))
+        s2 += (np.asarray(o.step_losses, dtype=np.float64) ** 2).sum(axis=(0, 1))
+    tot = np.concatenate(o_lane).sum(axis=0)
+    assert_sum_close("losses", np_out(out.losses)[1:], tot, np.sqrt(s2))
 
 
 EDGE_SHAPES = [
