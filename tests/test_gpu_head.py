@@ -230,6 +230,46 @@ def test_head_matches_plain_kernel_on_its_outputs():
     assert_close("pg", np_out(out.pg_advantages), np_out(plain.pg_advantages), rtol=2e-5, atol=2e-6)
 
 
+def test_head_stress_every_lane():
+    """The full stress shape with (1, 1, 1): every per-step and per-lane output
+    against the oracle, 512 lanes at a time, and d_W, d_b and the loss totals
+    against the oracle's sums over all chunks (the sum bound, with the RSS of
+    all their terms)."""
+    from synth import SEED_BASE, head_batch_from_device, make_head_device
+    c = HEAD_CONFIGS["stress"]
+    log_case("head stress, every lane: generating on the device")
+    d = make_head_device(c["T"], c["B"], c["A"], c["H"], SEED_BASE + 1004, "cuda")
+    dev = dict(hidden=d["hidden"], head_weight=d["weight"], head_bias=d["bias"],
+               behaviour_logits=d["behaviour_logits"], actions=d["actions"], rewards=d["rewards"],
+               discounts=d["discounts"], bootstrap_value=d["bootstrap_value"])
+    p = Params(1.0, 1.0, 1.0)
+    out = vt.vtrace_head_loss_grad(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
+                                   with_vs=True, with_pg_advantages=True, with_lane_losses=True,
+                                   with_outputs=True)
+    torch.cuda.synchronize()
+    C = c["A"] + 1
+    dw = np.zeros((c["H"], C)); db = np.zeros(C); tot = np.zeros(3)
+    rw2 = np.zeros((c["H"], C)); rb2 = np.zeros(C); s2 = np.zeros(3)
+    for l0 in range(0, c["B"], 512):
+        lanes = list(range(l0, min(c["B"], l0 + 512)))
+        log_case(f"head stress, lanes {l0}..{lanes[-1]}")
+        hb = head_batch_from_device(d, lanes)
+        sel = torch.as_tensor(lanes, device="cuda")
+        view = vt.HeadLossGrad(out.losses, out.d_hidden[:, sel].cpu(), out.d_weight, out.d_bias,
+                               out.vs[:, sel].cpu(), out.pg_advantages[:, sel].cpu(),
+                               out.lane_losses[sel], out.outputs[:, sel].cpu())
+        o = check_head(hb, p, view, whole=False)
+        rw, rb = oracle.sum_term_scale(hb.hidden, o.d_outputs)
+        dw += o.d_weight; db += o.d_bias; tot += o.losses[1:]
+        rw2 += rw ** 2; rb2 += rb ** 2; s2 += (o.step_losses ** 2).sum(axis=(0, 1))
+    assert_sum_close("d_weight", np_out(out.d_weight), dw, np.sqrt(rw2))
+    assert_sum_close("d_bias", np_out(out.d_bias), db, np.sqrt(rb2))
+    assert_sum_close("losses", np_out(out.losses),
+                     np.concatenate([[tot.sum()], tot]), np.sqrt(np.concatenate([[s2.sum()], s2])))
+    del out, d, dev
+    torch.cuda.empty_cache()
+
+
 def test_head_stress_sampled_lanes():
     """The full stress shape (T=1000, B=16384, A=18, H=256), drawn on the
     device, in the launch configuration the benchmark times; the oracle runs
