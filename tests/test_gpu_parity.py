@@ -96,14 +96,16 @@ def test_stress_subset_matches_oracle(stress, pidx):
     assert losses[0] == pytest.approx(losses[1:].sum(), rel=1e-6)
 
 
-def test_stress_every_lane_matches_oracle(stress):
-    """The full stress launch (T=1000, B=16384, A=18; the multi-tile walk) with
-    (1, 1, 1), every output element against the oracle, which runs on 2048
-    lanes at a time to bound host memory (lane losses and totals with the sum
-    bound); the totals against the fp64 sum of the oracle's lane losses."""
+@pytest.mark.parametrize("pidx", [0, 1, 2])
+def test_stress_every_lane_matches_oracle(stress, pidx):
+    """The full stress launch (T=1000, B=16384, A=18) with each parameter set
+    ((1, 1, 1) and (1, 0.5, 0.95) take the multi-tile walk, (inf, inf, 1) the
+    fp64 ratio mode), every output element against the oracle, which runs on
+    2048 lanes at a time to bound host memory (lane losses and totals with the
+    sum bound); the totals against the fp64 sum of the oracle's lane losses."""
     tr, dev = stress
-    p = PARAM_SETS[4][0]
-    log_case("stress T=1000 B=16384 A=18, every lane against the oracle")
+    p = PARAM_SETS[4][pidx]
+    log_case(f"stress T=1000 B=16384 A=18 {p.label()}, every lane against the oracle")
     out = run_loss_grad(dev, p)
     got = {k: np_out(getattr(out, k)) for k in ("vs", "pg_advantages", "d_values", "d_logits")}
     lane = np_out(out.lane_losses)
