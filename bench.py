@@ -35,7 +35,8 @@ METRIC = "trajectory steps/sec (T*B) for fused V-trace loss+grad; achieved HBM G
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "loss_grad_stress_counters.json")
 HEAD_COUNTERS_FILE = os.path.join(ROOT, "profiles", "head_stress_counters.json")
 # The sources each counted kernel is built from.
-PLAIN_SOURCES = ("tiled.hip", "tiled_impl.hpp", "row_stats.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
+PLAIN_SOURCES = ("tiled.hip", "tiled_long_f32.hip", "tiled_impl.hpp", "row_stats.hpp", "device_common.hpp",
+                 "wave_ops.hpp", "launch.hpp")
 HEAD_SOURCES = ("head.hip", "head.hpp", "device_common.hpp", "wave_ops.hpp", "launch.hpp")
 
 
@@ -47,10 +48,11 @@ def parse_args():
     ap.add_argument("--config", type=int, default=4, help="synthetic workload id (0-4)")
     ap.add_argument("--params", type=int, default=0, help="parameter set of the workload")
     ap.add_argument("--bf16", action="store_true", help="bfloat16 logits")
-    ap.add_argument("--kernel", choices=["auto", "lane_serial", "tiled", "tiled_single", "wide"],
+    ap.add_argument("--kernel", choices=["auto", "lane_serial", "tiled", "tiled_single", "tiled_short",
+                                         "tiled_short_single", "wide"],
                     default="auto",
                     help="force one V-trace kernel (where it applies); tiled_single keeps the tiled "
-                         "kernel to one workgroup per tile")
+                         "kernel to one workgroup per tile, tiled_short to its 16-step tiles")
     ap.add_argument("--correction", choices=["vtrace", "none", "epsilon", "one_step_is"],
                     default="vtrace")
     ap.add_argument("--log-probs", action="store_true",

@@ -44,16 +44,20 @@ bool dtype_of(vtrace_dtype d, LogitsType* lt) {
 
 // Kernel choice: the time-parallel kernel for short unrolls of small batches,
 // the tiled kernel where it applies, else the generic one.  VTRACE_KERNEL
-// (lane_serial, tiled, tiled_single or wide) forces a kernel where it applies,
-// to cross-check them; tiled_single is the tiled kernel with one workgroup per
-// tile, never the multi-tile walk.
-enum class Kernel { Auto, LaneSerial, Tiled, TiledSingle, Wide };
+// (lane_serial, tiled, tiled_single, tiled_short, tiled_short_single or wide)
+// forces a kernel where it applies, to cross-check them: tiled_single is the
+// tiled kernel with one workgroup per tile, never the multi-tile walk;
+// tiled_short keeps its 16-step tiles, never the long-run tile shapes;
+// tiled_short_single both.
+enum class Kernel { Auto, LaneSerial, Tiled, TiledSingle, TiledShort, TiledShortSingle, Wide };
 Kernel forced_kernel() {
   const char* k = std::getenv("VTRACE_KERNEL");
   if (k == nullptr) return Kernel::Auto;
   if (std::strcmp(k, "lane_serial") == 0) return Kernel::LaneSerial;
   if (std::strcmp(k, "tiled") == 0) return Kernel::Tiled;
   if (std::strcmp(k, "tiled_single") == 0) return Kernel::TiledSingle;
+  if (std::strcmp(k, "tiled_short") == 0) return Kernel::TiledShort;
+  if (std::strcmp(k, "tiled_short_single") == 0) return Kernel::TiledShortSingle;
   if (std::strcmp(k, "wide") == 0) return Kernel::Wide;
   return Kernel::Auto;
 }
@@ -181,7 +185,8 @@ vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s)
   else if (wide && (k == Kernel::Wide || (k == Kernel::Auto && prefer_wide(a))))
     e = vtrace::launch_wide(a, lt, mode, s, &nwg);
   else if (tiled)
-    e = vtrace::launch_tiled(a, lt, mode, s, &nwg, k != Kernel::TiledSingle);
+    e = vtrace::launch_tiled(a, lt, mode, s, &nwg, k != Kernel::TiledSingle && k != Kernel::TiledShortSingle,
+                             k != Kernel::TiledShort && k != Kernel::TiledShortSingle);
   else
     e = vtrace::launch_lane_serial(a, lt, mode, s, &nwg);
   return e == hipSuccess ? VTRACE_OK : VTRACE_ERR_HIP;

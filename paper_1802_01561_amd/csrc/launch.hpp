@@ -64,8 +64,16 @@ bool tiled_supported(const StepArgs& a, LogitsType lt);
 // prefetch no longer fits the registers of two waves per SIMD).  allow_multi
 // false keeps one workgroup per tile (no multi-tile walk).
 constexpr int64_t kTiledMaxActions = 20;
+// allow_long false keeps the 16-step tiles of 16 or 32 lanes (no long-run
+// tile shapes).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
-                        int64_t* num_workgroups, bool allow_multi);
+                        int64_t* num_workgroups, bool allow_multi, bool allow_long);
+// Long-run tile shapes for A = 9 and A = 18 in the float32 ratio mode: true
+// (with the launch status in *err) when one applies and was launched.
+bool launch_tiled_long_f32(const StepArgs& a, Mode mode, hipStream_t s, int64_t* num_workgroups,
+                           bool allow_multi, hipError_t* err);
+bool launch_tiled_long_bf16(const StepArgs& a, Mode mode, hipStream_t s, int64_t* num_workgroups,
+                            bool allow_multi, hipError_t* err);
 hipError_t launch_tiled_a2_8(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                              int64_t* num_workgroups, bool allow_multi);
 hipError_t launch_tiled_a10_14(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,

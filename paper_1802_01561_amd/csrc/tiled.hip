@@ -20,8 +20,18 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A >= 2 && a.A <= 
 // with 16; 16384 lanes 593 -> 558 us and 32768 lanes 1.23 -> 1.10 ms with 32),
 // and 32 when the whole batch is one tile (one workgroup, whose loss sums need
 // no cross-workgroup reduction).
+//
+// Batches that fill the chip in whole generations take the long-run shapes of
+// tiled_long_f32.hip / tiled_long_bf16.hip first.
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
-                        int64_t* num_workgroups, bool allow_multi) {
+                        int64_t* num_workgroups, bool allow_multi, bool allow_long) {
+  if (allow_long && (a.A == 9 || a.A == 18)) {
+    hipError_t err = hipSuccess;
+    const bool launched = lt == LogitsType::F32
+                              ? launch_tiled_long_f32(a, mode, st, num_workgroups, allow_multi, &err)
+                              : launch_tiled_long_bf16(a, mode, st, num_workgroups, allow_multi, &err);
+    if (launched) return err;
+  }
   if (lt == LogitsType::F32) {
     if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups, allow_multi);
     if (a.A == 9) {

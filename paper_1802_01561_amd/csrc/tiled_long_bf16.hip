@@ -1,0 +1,21 @@
+// Long-run tile shapes for bfloat16 logits, A = 9 and A = 18 (the kernel is in
+// tiled_impl.hpp).  Measured at T = 1000 against the 16-step tiles: A = 18,
+// 16384 lanes 0.572 -> 0.507 ms (64 lanes x 8 steps), 32768 lanes 1.12 ->
+// 0.98 ms (128 x 4); A = 9, 16384 lanes 0.435 -> 0.348 ms (32 x 8), 32768
+// lanes 0.788 -> 0.632 ms (64 x 4).  For A = 9 the 512-thread shapes measured
+// slower than these (one workgroup per CU).
+#include "tiled_impl.hpp"
+
+namespace vtrace {
+
+bool launch_tiled_long_bf16(const StepArgs& a, Mode mode, hipStream_t st, int64_t* num_workgroups,
+                            bool allow_multi, hipError_t* err) {
+  if (a.A == 18)
+    return launch_long<18, uint16_t, Shape<128, 4>, Shape<64, 8>, Shape<64, 4>>(a, mode, st, num_workgroups,
+                                                                               allow_multi, err);
+  if (a.A == 9)
+    return launch_long<9, uint16_t, Shape<64, 4>, Shape<32, 8>>(a, mode, st, num_workgroups, allow_multi, err);
+  return false;
+}
+
+}  // namespace vtrace

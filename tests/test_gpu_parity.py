@@ -384,12 +384,12 @@ def _bits(t):
 @pytest.mark.parametrize("A,bf16,grad", [(18, False, "float32"), (18, False, "bfloat16"),
                                          (9, True, "bfloat16"), (9, True, "float32")])
 def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
-    """A batch whose tile count is a whole multiple (at least two) of the
-    workgroups the chip holds at once runs the tiled kernel's multi-tile walk
-    (for the kernels that fit two or more workgroups per CU: fp32 logits with
-    A = 18 and bf16 logits with A = 9; fp32 A = 9 takes 32-lane tiles at this
-    size and bf16 A = 18 fits one workgroup per CU); on a 256-CU part
-    B = 24576 is such a batch.
+    """With the 16-step tiles (VTRACE_KERNEL=tiled_short), a batch whose tile
+    count is a whole multiple (at least two) of the workgroups the chip holds
+    at once runs the tiled kernel's multi-tile walk (for the kernels that fit
+    two or more workgroups per CU: fp32 logits with A = 18 and bf16 logits with
+    A = 9; fp32 A = 9 takes 32-lane tiles at this size and bf16 A = 18 fits one
+    workgroup per CU); on a 256-CU part B = 24576 is such a batch.
     Every per-step and per-lane output must be bit-identical to the walk with
     one workgroup per tile (the same arithmetic per lane; only the order of the
     batch totals differs), the totals must agree within the sum tolerance, and
@@ -402,10 +402,10 @@ def test_multi_tile_walk_matches_single_tile(A, bf16, grad, monkeypatch):
                        + list(range(511, B, 4093))))
     for p in (PARAM_SETS[4][0], PARAM_SETS[4][2]):
         log_case(f"multi-tile walk T={T} B={B} A={A} bf16={bf16} grad={grad} {p.label()}")
-        monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled_short")
         a = run_loss_grad(dev, p, grad_dtype=gd)
         ta = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
-        monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled_short_single")
         b = run_loss_grad(dev, p, grad_dtype=gd)
         tb = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
         torch.cuda.synchronize()
@@ -498,14 +498,56 @@ def test_multi_tile_walk_unroll_lengths(T, monkeypatch):
     dev = to_device(tr)
     p = PARAM_SETS[4][0]
     log_case(f"multi-tile walk T={T} B={B} A={A}")
-    monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+    monkeypatch.setenv("VTRACE_KERNEL", "tiled_short")
     a = run_loss_grad(dev, p)
-    monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+    monkeypatch.setenv("VTRACE_KERNEL", "tiled_short_single")
     b = run_loss_grad(dev, p)
     monkeypatch.delenv("VTRACE_KERNEL")
     for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses"):
         assert np.array_equal(_bits(getattr(a, name)), _bits(getattr(b, name))), name
     check_against_oracle(tr, p, a, lanes=[0, 15, 16, 8191, 8192, B - 17, B - 1])
+
+
+@pytest.mark.parametrize("A,bf16", [(18, False), (9, False), (18, True), (9, True)])
+@pytest.mark.parametrize("lanes_per_cu", [64, 128, 256])
+def test_long_run_tile_shapes(A, bf16, lanes_per_cu, monkeypatch):
+    """Batches of 64, 128 and 256 lanes per CU take the long-run tile shapes
+    where the float32 ratio mode applies (64 x 8, 128 x 4 or 64 x 4 lanes x
+    steps per chunk, and 32 x 8 or 64 x 4 for bf16 logits with A = 9; 64 x 4
+    through the multi-tile walk where the batch is a whole number of its
+    generations).  T = 37 leaves every chunk length a ragged last chunk.  Every
+    output against the oracle, with weights clipped at 1, with (1, 0.5, 0.95),
+    and unclipped (which takes the float64 ratio mode and the 16-step tiles);
+    the targets-only call against the oracle; the 16-step tiles
+    (VTRACE_KERNEL=tiled_short) within the tolerance; and one workgroup per tile
+    (tiled_single, the same shape without the multi-tile walk) bit-identical
+    per step and per lane."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    T, B = 37, lanes_per_cu * cus
+    tr = make_random(T, B, A, 3000 + A + lanes_per_cu, noise_std=1.0, end_prob=0.03, bf16=bf16)
+    dev = to_device(tr)
+    for p in (PARAM_SETS[4][0], PARAM_SETS[4][2], PARAM_SETS[4][1]):
+        log_case(f"long-run tiles T={T} B={B} A={A} bf16={bf16} {p.label()}")
+        monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+        a = run_loss_grad(dev, p)
+        o = check_against_oracle(tr, p, a)
+        tv, tp = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
+        torch.cuda.synchronize()
+        assert_close("targets vs", np_out(tv), o.vs)
+        assert_close("targets pg_advantages", np_out(tp), o.pg_advantages)
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled_short")
+        b = run_loss_grad(dev, p)
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+        c = run_loss_grad(dev, p)
+        monkeypatch.delenv("VTRACE_KERNEL")
+        for name in ("vs", "pg_advantages", "d_values", "d_logits"):
+            assert_close(f"long-run vs 16-step tiles {name}", np_out(getattr(a, name)),
+                         np_out(getattr(b, name)), rtol=2e-5, atol=2e-6)
+        for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses"):
+            assert np.array_equal(_bits(getattr(a, name)), _bits(getattr(c, name))), \
+                f"{name} differs between the multi-tile walk and one workgroup per tile"
+    del dev
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("kernel", ["tiled", "wide"])
