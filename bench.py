@@ -114,15 +114,40 @@ def calibrate_copy(mib, reps):
                       "add_2read_1write_GBps": 3 * n * 4 / mix_ms / 1e6}), flush=True)
 
 
+def code_tokens(text: str) -> str:
+    """C++ source with comments removed and whitespace runs collapsed: what the
+    compiler sees, so that editing a comment keeps stored counters valid."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_digest(files=PLAIN_SOURCES) -> str:
-    """Hash of the HIP sources a kernel is built from, to tell whether stored
-    counters still describe it."""
+    """Hash of the code (comments and layout aside) of the HIP sources a kernel
+    is built from, to tell whether stored counters still describe it."""
     csrc = os.path.join(ROOT, "paper_1802_01561_amd", "csrc")
     h = hashlib.sha256()
     for f in sorted(files):
         h.update(f.encode())
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(code_tokens(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

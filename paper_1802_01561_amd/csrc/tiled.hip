@@ -21,8 +21,9 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A >= 2 && a.A <= 
 // and 32 when the whole batch is one tile (one workgroup, whose loss sums need
 // no cross-workgroup reduction).
 //
-// Batches that fill the chip in whole generations take the long-run shapes of
-// tiled_long_f32.hip / tiled_long_bf16.hip first.
+// These are the shapes with 16-step chunks.  Batches of A = 9 or 18 that fill
+// the chip in whole generations take the long-run shapes of tiled_long_f32.hip
+// and tiled_long_bf16.hip first (64 or 128 lanes, chunks of 8 or 4 steps).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups, bool allow_multi, bool allow_long) {
   if (allow_long && (a.A == 9 || a.A == 18)) {

@@ -3,16 +3,18 @@
 // A = 18 the full Atari set).
 //
 // Work split.  A tile is LANES consecutive lanes (batch entries) for the whole
-// unroll; a workgroup walks a tile's time backwards in chunks of L = 16 steps,
-// so every carry of the reverse recursion stays inside the workgroup.  Within
-// a chunk, thread (lane, s) handles step t = t0 + s; the 16 threads of one lane
-// are one DPP row of a wave.  When the batch has a whole multiple of the tiles
-// the chip holds workgroups at once, each resident workgroup walks an equal
-// share of tiles as one continuous sequence of chunks.
+// unroll; a workgroup walks a tile's time backwards in chunks of L steps (16 by
+// default; 8 or 4 for the long-run tile shapes of 64 or 128 lanes), so every
+// carry of the reverse recursion stays inside the workgroup.  Within a chunk,
+// thread (lane, s) handles step t = t0 + s; the L threads of one lane are an
+// aligned segment of a 16-lane DPP row of a wave.  When the batch has a whole
+// multiple of the tiles the chip holds workgroups at once, each resident
+// workgroup walks an equal share of tiles as one continuous sequence of chunks.
 //
 // Data path per chunk.
 //  1. For each t the chunk's logits are one contiguous run of LANES*A elements
-//     (1152 bytes for fp32 logits: nine 128-byte lines).  Threads copy both
+//     (1152 bytes for 16 lanes of fp32 logits with A = 18, nine 128-byte
+//     lines; 4608 bytes for 64 lanes).  Threads copy both
 //     tensors' runs with 16-byte loads into LDS.  These whole-line logit loads
 //     and the gradient stores are used once, so they carry the non-temporal
 //     hint; the [T,B] scalars, whose 64-byte halves neighbouring workgroups

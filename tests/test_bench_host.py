@@ -48,6 +48,22 @@ def test_digest_follows_the_kernel_sources(tmp_path, monkeypatch):
     assert bench.stored_traffic(1.0, str(tmp_path / "missing.json")) == (None, None)
 
 
+def test_digest_ignores_comments_not_code(tmp_path, monkeypatch):
+    csrc = tmp_path / "paper_1802_01561_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    src = csrc / "k.hip"
+
+    def digest(text):
+        src.write_text(text)
+        return bench.kernel_source_digest(("k.hip",))
+
+    base = digest('int f() { return 1; }  // one\nconst char* s = "a // b";\n')
+    assert digest('/* doc */ int f()  {\n  return 1;  // the value one\n}\nconst char* s = "a // b";') == base
+    assert digest('int f() { return 2; }  // one\nconst char* s = "a // b";\n') != base
+    assert digest('int f() { return 1; }  // one\nconst char* s = "a // c";\n') != base
+
+
 def test_committed_counters_are_well_formed():
     for name in ("loss_grad_stress_counters.json", "head_stress_counters.json"):
         c = json.load(open(os.path.join(ROOT, "profiles", name)))
