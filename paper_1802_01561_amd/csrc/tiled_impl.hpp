@@ -77,7 +77,11 @@ struct Tile {
   static constexpr int SCAN = L == 16 ? 4 : L == 8 ? 3 : 2;  // suffix-scan stages, log2 L
   static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;  // vectors per thread, both tensors
   static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;     // gradient vectors per thread
-  static constexpr int LDS16 = (2 * IN_LDS16 > OUT_LDS16) ? 2 * IN_LDS16 : OUT_LDS16;
+  // LDS: the two logit tiles, and for the gradient kernels a separate
+  // staging tile for the gradient rows, so that a chunk needs two barriers
+  // (logits staged; gradients staged) instead of four.
+  static constexpr int LDS16_TARGETS = 2 * IN_LDS16;
+  static constexpr int LDS16_GRAD = 2 * IN_LDS16 + OUT_LDS16;
   static constexpr int IN_PITCH = IN_PITCH16 * 16 / int(sizeof(In));  // elements per LDS row
   static constexpr int OUT_PITCH = OUT_PITCH16 * 4;                    // floats per LDS row
   static_assert((SEG * int(sizeof(In))) % 16 == 0, "logit rows must be whole 16-byte vectors");
@@ -108,6 +112,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   constexpr int NT = S::NT;
   v4u* const lds_z = lds;
   v4u* const lds_y = lds + S::IN_LDS16;
+  v4u* const lds_g = lds + 2 * S::IN_LDS16;  // gradient staging (kGrad)
 
   const int tid = threadIdx.x;
   const int lane_local = tid / L;
@@ -196,7 +201,10 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const bool step_ok = lane_ok && t >= 0;
     const int64_t idx = t * B + b;
 
-    __syncthreads();  // the previous chunk is done with LDS
+    // Every thread is past the previous chunk's row reads: the gradient
+    // kernels passed their staging barrier after them; the targets-only
+    // kernel waits here.
+    if constexpr (!kGrad) __syncthreads();
     int32_t act;
     float r32, g32, V32, lmu = 0.f;
     if constexpr (kVec) {
@@ -326,8 +334,9 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       float out[A_];
 #pragma unroll
       for (int j = 0; j < A_; ++j) out[j] = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
-      __syncthreads();  // every row has been read: LDS now takes the gradient tile
-      float* lo = reinterpret_cast<float*>(lds) + s * S::OUT_PITCH + lane_local * A_;
+      // The staging tile was last read by the previous chunk's stores, which
+      // every thread finished before this chunk's logits barrier.
+      float* lo = reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_;
 #pragma unroll
       for (int j = 0; j < A_; ++j) lo[j] = out[j];
       lo[act_c] = act_ok ? out_a : NAN;
@@ -342,7 +351,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
               const int rr = f / S::OUT_ROW16, cc = f % S::OUT_ROW16;
               if (rr >= neg)
                 __builtin_nontemporal_store(
-                    lds[rr * S::OUT_PITCH16 + cc],
+                    lds_g[rr * S::OUT_PITCH16 + cc],
                     reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
             }
           });
@@ -352,8 +361,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
           for (int f = tid; f < kTile16; f += NT) {
             const int rr = f / kRow16, cc = f % kRow16;
             if (rr >= neg) {
-              const v4u lo = lds[rr * S::OUT_PITCH16 + 2 * cc];
-              const v4u hi = lds[rr * S::OUT_PITCH16 + 2 * cc + 1];
+              const v4u lo = lds_g[rr * S::OUT_PITCH16 + 2 * cc];
+              const v4u hi = lds_g[rr * S::OUT_PITCH16 + 2 * cc + 1];
               v4u pk;
               pk.x = pack_bf16x2(__uint_as_float(lo.x), __uint_as_float(lo.y));
               pk.y = pack_bf16x2(__uint_as_float(lo.z), __uint_as_float(lo.w));
@@ -365,7 +374,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
           }
         }
       } else {
-        const float* lf = reinterpret_cast<const float*>(lds);
+        const float* lf = reinterpret_cast<const float*>(lds_g);
         for (int e2 = tid; e2 < L * S::SEG; e2 += NT) {
           const int rr = e2 / S::SEG, cc = e2 % S::SEG;
           const int64_t te = t0 + rr;
@@ -427,7 +436,7 @@ __global__ __launch_bounds__(LANES* L, (kPrecise && A_ > 18) ? 2 : 1) void tiled
     StepArgs a, int64_t num_vec_tiles, int64_t tiles_per_wg) {
   using S = Tile<A_, LANES, In, L>;
   constexpr int NT = S::NT;
-  __shared__ v4u lds[S::LDS16];
+  __shared__ v4u lds[kGrad ? S::LDS16_GRAD : S::LDS16_TARGETS];
   __shared__ double red_scratch[3 * (NT / kWave)];
 
   const int lane_local = threadIdx.x / L;
