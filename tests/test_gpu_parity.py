@@ -580,13 +580,16 @@ def test_wide_kernel_shapes(T, B, A, monkeypatch):
             check_against_oracle(tr, p, run_loss_grad(to_device(tr), p))
 
 
-def test_offsets_beyond_four_gib():
-    """Logit tensors larger than 2^32 bytes (T=64, B=2^20+8, A=18: 4.8 GB each):
-    byte offsets need more than 32 bits, signed or not.  Rows stay 16-byte
-    aligned, so all but the last, ragged workgroup take the vector path; the
-    oracle checks lanes spread over the batch, including the last ones, whose
-    elements lie beyond 2^32 bytes."""
-    T, B, A = 64, (1 << 20) + 8, 18
+@pytest.mark.parametrize("B", [(1 << 20) + 8, 1 << 20])
+def test_offsets_beyond_four_gib(B):
+    """Logit tensors larger than 2^32 bytes (T=64, B=2^20+8 or 2^20, A=18:
+    4.8 GB each): byte offsets need more than 32 bits, signed or not.  With
+    2^20 + 8 lanes rows stay 16-byte aligned, so all but the last, ragged
+    workgroup take the vector path of the 16-step tiles; 2^20 lanes are a whole
+    number of generations of the 64 x 4 long-run tiles, which take the
+    multi-tile walk (on a 256-CU part).  The oracle checks lanes spread over
+    the batch, including the last ones, whose elements lie beyond 2^32 bytes."""
+    T, A = 64, 18
     assert T * B * A * 4 > 2**32
     log_case(f"large batch T={T} B={B} A={A} ({T * B * A * 4 / 2**30:.2f} GiB per logit tensor)")
     tr = make_random(T, B, A, 4321, noise_std=1.0, end_prob=0.01)
