@@ -655,27 +655,53 @@ bool walks_evenly(int64_t B, int cus) {
   return resident >= 2 * static_cast<int64_t>(cus) && tiles >= 2 * resident && tiles % resident == 0;
 }
 
+// One workgroup per tile runs the batch as 2 to kMaxGenerations whole
+// generations of resident workgroups, each CU holding at least kMinWavesPerCu
+// waves.  (Measured up to four generations.)
+constexpr int64_t kMaxGenerations = 4;
+template <int A_, typename In, bool kGrad, typename Sh>
+bool whole_generations(int64_t B, int cus) {
+  if (B % Sh::LANES != 0) return false;
+  const int64_t tiles = B / Sh::LANES;
+  const int per_cu = single_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kGrad>();
+  const int64_t resident = static_cast<int64_t>(per_cu) * cus;
+  return per_cu * (Sh::LANES * Sh::L / kWave) >= kMinWavesPerCu && resident > 0 && tiles % resident == 0 &&
+         tiles >= 2 * resident && tiles <= kMaxGenerations * resident;
+}
+
+enum class ShapeTest { FillsOnce, WalksEvenly, WholeGenerations };
+
+template <int A_, typename In, bool kGrad, typename Sh>
+bool shape_fits(ShapeTest test, int64_t B, int cus) {
+  switch (test) {
+    case ShapeTest::FillsOnce: return fills_once<A_, In, kGrad, Sh>(B, cus);
+    case ShapeTest::WalksEvenly: return walks_evenly<A_, In, kGrad, Sh>(B, cus);
+    case ShapeTest::WholeGenerations: return whole_generations<A_, In, kGrad, Sh>(B, cus);
+  }
+  return false;
+}
+
 template <int A_, typename In>
-bool try_shapes(const StepArgs&, Mode, hipStream_t, int64_t*, bool, hipError_t*, int, bool) {
+bool try_shapes(const StepArgs&, Mode, hipStream_t, int64_t*, bool, hipError_t*, int, ShapeTest) {
   return false;
 }
 template <int A_, typename In, typename Sh, typename... Rest>
 bool try_shapes(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi, hipError_t* err,
-                int cus, bool once) {
-  const bool grad = mode == Mode::LossGrad;
-  const bool ok = once ? (grad ? fills_once<A_, In, true, Sh>(a.B, cus) : fills_once<A_, In, false, Sh>(a.B, cus))
-                       : (grad ? walks_evenly<A_, In, true, Sh>(a.B, cus) : walks_evenly<A_, In, false, Sh>(a.B, cus));
+                int cus, ShapeTest test) {
+  const bool ok = mode == Mode::LossGrad ? shape_fits<A_, In, true, Sh>(test, a.B, cus)
+                                         : shape_fits<A_, In, false, Sh>(test, a.B, cus);
   if (ok) {
     *err = launch_shape<A_, Sh::LANES, In, Sh::L, true>(a, mode, st, nwg, allow_multi);
     return true;
   }
-  return try_shapes<A_, In, Rest...>(a, mode, st, nwg, allow_multi, err, cus, once);
+  return try_shapes<A_, In, Rest...>(a, mode, st, nwg, allow_multi, err, cus, test);
 }
 
 // Launches the first of Shapes (listed longest runs first) whose batch fills
 // the chip once, else the first that the multi-tile walk runs as even
 // generations (the choice does not depend on allow_multi, which only says
-// whether the walk may run); returns false (launching nothing) when none
+// whether the walk may run), else the first whose single-tile workgroups run
+// it as a few whole generations; returns false (launching nothing) when none
 // applies or the ratio needs the float64 mode (where the 16-step chunks of the
 // default shapes measured as fast or faster).
 template <int A_, typename In, typename... Shapes>
@@ -683,8 +709,9 @@ bool launch_long(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, boo
   if (ratio_needs_fp64(a)) return false;
   const int cus = compute_units();
   if (cus <= 0) return false;
-  return try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, true) ||
-         try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, false);
+  return try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::FillsOnce) ||
+         try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::WalksEvenly) ||
+         try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::WholeGenerations);
 }
 
 // Launch for action count A with 16 lanes per workgroup, fp32 or bf16 logits.

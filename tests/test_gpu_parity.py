@@ -509,13 +509,14 @@ def test_multi_tile_walk_unroll_lengths(T, monkeypatch):
 
 
 @pytest.mark.parametrize("A,bf16", [(18, False), (9, False), (18, True), (9, True)])
-@pytest.mark.parametrize("lanes_per_cu", [64, 128, 256])
+@pytest.mark.parametrize("lanes_per_cu", [64, 128, 192, 256])
 def test_long_run_tile_shapes(A, bf16, lanes_per_cu, monkeypatch):
-    """Batches of 64, 128 and 256 lanes per CU take the long-run tile shapes
-    where the float32 ratio mode applies (64 x 8, 128 x 4 or 64 x 4 lanes x
-    steps per chunk, and 32 x 8 or 64 x 4 for bf16 logits with A = 9; 64 x 4
-    through the multi-tile walk where the batch is a whole number of its
-    generations).  T = 37 leaves every chunk length a ragged last chunk.  Every
+    """Batches of 64, 128, 192 and 256 lanes per CU take the long-run tile
+    shapes where the float32 ratio mode applies (64 x 8, 128 x 4 or 64 x 4
+    lanes x steps per chunk, and 32 x 8 or 64 x 4 for bf16 logits with A = 9;
+    64 x 4 through the multi-tile walk where the batch is a whole number of its
+    generations; 192 lanes per CU as three generations of 64 x 8 for fp32
+    logits).  T = 37 leaves every chunk length a ragged last chunk.  Every
     output against the oracle, with weights clipped at 1, with (1, 0.5, 0.95),
     and unclipped (which takes the float64 ratio mode and the 16-step tiles);
     the targets-only call against the oracle; the 16-step tiles
