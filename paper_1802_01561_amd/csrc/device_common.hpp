@@ -36,6 +36,16 @@ __device__ __forceinline__ double importance_ratio(float za, float mz, float ya,
 constexpr int kCorrVtrace = 0, kCorrNone = 1, kCorrEpsilon = 2, kCorrOneStepIs = 3;
 constexpr int kQBaseline = 1;  // StepArgs::q_estimate: q_s = r_s + gamma_s V(x_{s+1})
 
+// Which ratio mode a call takes (the same rule for every kernel; Args is
+// StepArgs or HeadArgs).  float32 ratios suffice unless V-trace's weights can
+// exceed 1: products of c can then grow and amplify rounding (lambda c_bar > 1),
+// or rho is left unclipped above 1.  The other variants use the ratio, if at
+// all, only as one factor of one step's advantage.
+template <typename Args>
+inline bool ratio_needs_fp64(const Args& a) {
+  return a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
+}
+
 // The weights a step contributes under a correction variant: rho and c in the
 // value target, and the weight on the advantage.  V-trace uses the truncated
 // rho_t and c_t everywhere; the uncorrected variants use rho = 1 and c = lambda

@@ -729,8 +729,7 @@ __global__ __launch_bounds__(kFinishWaves* kWave) void head_finish_kernel(HeadAr
 
 template <int H, int NT, typename BehIn, bool kBf16Grad>
 void launch_head_grad(const HeadArgs& a, hipStream_t st, unsigned nwg) {
-  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
-  if (precise)
+  if (ratio_needs_fp64(a))
     hipLaunchKernelGGL((head_kernel<H, NT, true, BehIn, kBf16Grad>), dim3(nwg), dim3(kHeadThreads), 0, st, a);
   else
     hipLaunchKernelGGL((head_kernel<H, NT, false, BehIn, kBf16Grad>), dim3(nwg), dim3(kHeadThreads), 0, st, a);

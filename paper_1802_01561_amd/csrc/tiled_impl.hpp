@@ -589,13 +589,6 @@ int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t 
   return tiles;
 }
 
-// float32 ratios suffice unless V-trace's weights can exceed 1 (products of c
-// can then grow and amplify rounding).  The other variants use the ratio, if at
-// all, only as one factor of one step's advantage.
-inline bool ratio_needs_fp64(const StepArgs& a) {
-  return a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
-}
-
 // kFastOnly: only the float32 ratio mode is instantiated (the caller has
 // checked ratio_needs_fp64).
 template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly>

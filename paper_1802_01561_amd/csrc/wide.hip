@@ -185,8 +185,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
 
 template <int A_, typename In, bool kGrad>
 void launch_wide_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int tp_log2) {
-  const bool precise = a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
-  if (precise)
+  if (ratio_needs_fp64(a))
     hipLaunchKernelGGL((wide_kernel<A_, In, kGrad, true>), dim3(blocks), dim3(kWideThreads), 0, st, a,
                        tp_log2);
   else
