@@ -551,6 +551,34 @@ def test_long_run_tile_shapes(A, bf16, lanes_per_cu, monkeypatch):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("lanes_per_cu,T", [(64, 1), (64, 7), (64, 8), (64, 9), (128, 1), (128, 3),
+                                             (128, 4), (128, 5), (256, 1), (256, 4), (256, 5)])
+def test_long_run_tile_shapes_short_unrolls(lanes_per_cu, T, monkeypatch):
+    """Unrolls of at most one chunk of the long-run shapes (fp32 logits, A = 18:
+    64 x 8 at 64 lanes per CU, 128 x 4 at 128, 64 x 4 with the multi-tile walk
+    at 256), exactly one chunk, and one step more: the only chunk starting
+    before t = 0, and in the multi-tile walk a tile's carry reset and lane
+    totals in the same iteration.  Every output against the oracle, and the
+    multi-tile walk bit-identical per step and per lane to one workgroup per
+    tile."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    A, B = 18, lanes_per_cu * cus
+    tr = make_random(T, B, A, 3100 + T + lanes_per_cu, noise_std=1.0, end_prob=0.05)
+    dev = to_device(tr)
+    p = PARAM_SETS[4][0]
+    log_case(f"long-run tiles, short unroll T={T} B={B} A={A}")
+    monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+    a = run_loss_grad(dev, p)
+    check_against_oracle(tr, p, a)
+    monkeypatch.setenv("VTRACE_KERNEL", "tiled_single")
+    b = run_loss_grad(dev, p)
+    monkeypatch.delenv("VTRACE_KERNEL")
+    for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses"):
+        assert np.array_equal(_bits(getattr(a, name)), _bits(getattr(b, name))), name
+    del dev
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
                                       (2, True)])
