@@ -337,9 +337,9 @@ def run_head(args):
     import torch
 
     import paper_1802_01561_amd as vt
-    from synth import HEAD_CONFIGS, SEED_BASE, Params, make_head_device
+    from synth import HEAD_WORKLOADS, SEED_BASE, Params, make_head_device
 
-    c = HEAD_CONFIGS["stress"]
+    c = HEAD_WORKLOADS["stress"]
     T, B, A, H = c["T"], c["B"], c["A"], c["H"]
     seed = SEED_BASE + 1004
     p = Params()
@@ -420,7 +420,7 @@ def run_head(args):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path. Lanes are "
+        print("bench.py measures one GPU only: the library has no multi-GPU path. Lanes are "
               "independent, so the batch axis would shard across GPUs with no communication "
               "except a 4-float loss all-reduce.", file=sys.stderr)
         sys.exit(2)

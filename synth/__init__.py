@@ -6,7 +6,7 @@ the HIP path consume what it produces, and neither imports the other.
 """
 
 from .trajectories import (  # noqa: F401
-    CONFIGS,
+    WORKLOADS,
     PARAM_SETS,
     SEED_BASE,
     Params,
@@ -18,7 +18,7 @@ from .trajectories import (  # noqa: F401
     subset_lanes,
 )
 from .head import (  # noqa: F401
-    HEAD_CONFIGS,
+    HEAD_WORKLOADS,
     HeadBatch,
     head_batch_from_device,
     make_head,

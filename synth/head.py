@@ -38,7 +38,7 @@ from .trajectories import SEED_BASE, _gumbel_argmax, bf16_bits_to_f32, f32_to_bf
 
 TANH_SQ_MEAN = 0.394  # E[tanh(X)^2] for X ~ N(0, 1), to three digits
 
-HEAD_CONFIGS = {
+HEAD_WORKLOADS = {
     "tiny": dict(T=5, B=4, A=9, H=64),
     "dmlab": dict(T=100, B=32, A=9, H=256),
     "atari": dict(T=20, B=32, A=18, H=256),
@@ -96,10 +96,10 @@ def make_head(T: int, B: int, A: int, H: int, seed: int, *, behaviour_std: float
 
 
 def make_head_config(name: str) -> HeadBatch:
-    c = HEAD_CONFIGS[name]
+    c = HEAD_WORKLOADS[name]
     if name == "stress":
         raise ValueError("the stress head batch is drawn on the device: make_head_device")
-    seed = SEED_BASE + 1000 + list(HEAD_CONFIGS).index(name)
+    seed = SEED_BASE + 1000 + list(HEAD_WORKLOADS).index(name)
     return make_head(c["T"], c["B"], c["A"], c["H"], seed)
 
 

@@ -92,7 +92,7 @@ class Trajectories:
         return self.target_logits, self.behaviour_logits
 
 
-CONFIGS = {
+WORKLOADS = {
     0: dict(name="tiny", T=5, B=4, A=9),
     1: dict(name="dmlab", T=100, B=32, A=9),
     2: dict(name="atari", T=20, B=32, A=18),
@@ -218,7 +218,7 @@ def _generate(name, T, B, A, seed, *, noise_std, reward_kind, end_prob,
 
 def make_config(cfg: int, bf16: bool = False) -> Trajectories:
     """The five fixed workloads (tiny, DMLab-shaped, Atari-shaped, 30-task, stress)."""
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     seed = SEED_BASE + 10 * cfg
     name = c["name"] + ("_bf16" if bf16 else "")
     T, B, A = c["T"], c["B"], c["A"]

@@ -22,7 +22,7 @@ import torch
 import oracle
 import paper_1802_01561_amd as vt
 from gpu_util import ATOL, RTOL, assert_close, assert_sum_close, log_case, np_out, require_gpu
-from synth import HEAD_CONFIGS, Params, make_head, make_head_config, subset_head_lanes
+from synth import HEAD_WORKLOADS, Params, make_head, make_head_config, subset_head_lanes
 
 pytestmark = pytest.mark.gpu
 
@@ -236,7 +236,7 @@ def test_head_stress_every_lane():
     against the oracle's sums over all chunks (the sum bound, with the RSS of
     all their terms)."""
     from synth import SEED_BASE, head_batch_from_device, make_head_device
-    c = HEAD_CONFIGS["stress"]
+    c = HEAD_WORKLOADS["stress"]
     log_case("head stress, every lane: generating on the device")
     d = make_head_device(c["T"], c["B"], c["A"], c["H"], SEED_BASE + 1004, "cuda")
     dev = dict(hidden=d["hidden"], head_weight=d["weight"], head_bias=d["bias"],
@@ -276,7 +276,7 @@ def test_head_stress_sampled_lanes():
     on 64 lanes spread over the batch."""
     from synth import SEED_BASE, head_batch_from_device, make_head_device
     from synth.trajectories import STRESS_SUBSET
-    c = HEAD_CONFIGS["stress"]
+    c = HEAD_WORKLOADS["stress"]
     log_case("head stress: generating on the device")
     d = make_head_device(c["T"], c["B"], c["A"], c["H"], SEED_BASE + 1004, "cuda")
     dev = dict(hidden=d["hidden"], head_weight=d["weight"], head_bias=d["bias"],

@@ -9,7 +9,7 @@ import synth.trajectories as st
 def test_configs_shapes_and_determinism():
     for cfg in (0, 1, 2):
         a, b = make_config(cfg), make_config(cfg)
-        c = st.CONFIGS[cfg]
+        c = st.WORKLOADS[cfg]
         assert a.target_logits.shape == (c["T"], c["B"], c["A"])
         assert a.actions.dtype == np.int32 and a.actions.min() >= 0 and a.actions.max() < c["A"]
         for name in ("target_logits", "behaviour_logits", "actions", "rewards", "discounts",
@@ -57,7 +57,7 @@ def test_subset_lanes():
 
 
 def test_head_batches_are_seeded_and_shaped():
-    from synth import HEAD_CONFIGS, make_head, make_head_config, subset_head_lanes
+    from synth import HEAD_WORKLOADS, make_head, make_head_config, subset_head_lanes
     a = make_head(9, 5, 7, 64, 42)
     b = make_head(9, 5, 7, 64, 42)
     for f in ("hidden_bits", "weight_bits", "bias", "behaviour_logits", "actions", "rewards",
@@ -69,7 +69,7 @@ def test_head_batches_are_seeded_and_shaped():
     assert a.actions.min() >= 0 and a.actions.max() < 7
     assert set(np.unique(a.discounts)) <= {0.0, np.float32(0.99)}
     c = make_head_config("atari")
-    assert (c.T, c.B, c.A, c.H) == (HEAD_CONFIGS["atari"]["T"], 32, 18, 256)
+    assert (c.T, c.B, c.A, c.H) == (HEAD_WORKLOADS["atari"]["T"], 32, 18, 256)
     s = subset_head_lanes(c, [3, 0])
     np.testing.assert_array_equal(s.hidden_bits[:, 1], c.hidden_bits[:, 0])
     np.testing.assert_array_equal(s.bootstrap_value, c.bootstrap_value[[3, 0]])
