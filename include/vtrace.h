@@ -37,13 +37,16 @@
  *             (every v_s uses the rest of the unroll; v_T = V(x_T))
  *   pg_adv_s = rho_s (r_s + gamma_s v_{s+1} - V(x_s))
  *
- * Numerics.  Per-row softmax work is float32 and the recursion, advantages and
- * loss partial sums are float64.  The importance ratio is formed from float32
- * exponent sums while every weight is at most 1 (rho_bar <= 1 and
- * lambda * c_bar <= 1, where nothing amplifies its rounding), and from float64
- * exponentials and sums otherwise (V-trace with larger or no truncation, where
- * products of c_t can grow).  Outputs are float32 (or bfloat16 where a variant
- * asks for it).  NaN or Inf inputs are propagated, not sanitised.
+ * Numerics.  The recursion, advantages and loss partial sums are float64.  The
+ * exponent sums of both log-softmaxes, and from them the importance ratio and
+ * log pi(a_t|x_t), are float64 (float64 exponentials of exact differences,
+ * about 1e-10 relative) in every call that forms losses, and in a targets-only
+ * call whose weights can exceed 1 (V-trace with rho_bar > 1 or
+ * lambda * c_bar > 1, where products of c_t amplify the ratio's rounding).  A
+ * targets-only call with every weight at most 1 forms them from float32
+ * exponentials.  The per-element softmax work of the gradient and the entropy
+ * is float32.  Outputs are float32 (or bfloat16 where a variant asks for it).
+ * NaN or Inf inputs are propagated, not sanitised.
  *
  * Errors that only the device can see.  An action outside [0, A) makes that
  * step's importance ratio NaN; the NaN reaches that step's outputs, every

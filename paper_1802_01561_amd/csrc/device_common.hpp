@@ -20,18 +20,6 @@ __device__ __forceinline__ float logit_to_float(uint16_t bits) {
 // ratio stays NaN (fmin would return `bar`).  min(+inf, x) = x.
 __device__ __forceinline__ double clip_above(double x, double bar) { return x > bar ? bar : x; }
 
-// pi(a|x)/mu(a|x) from the max-shifted logits at the taken action and the two
-// exponent sums s = sum_j exp(l_j - max_j l_j):
-//   ratio = exp((z_a - m_z) - (y_a - m_y)) * s_mu / s_pi.
-// The differences of two floats are exact in float64, so the only float32
-// rounding left is in the exponentials that make up the sums.
-__device__ __forceinline__ double importance_ratio(float za, float mz, float ya, float my,
-                                                   double s_pi, double s_mu) {
-  const double dz = static_cast<double>(za) - static_cast<double>(mz);
-  const double dy = static_cast<double>(ya) - static_cast<double>(my);
-  return exp(dz - dy) * (s_mu / s_pi);
-}
-
 // Correction variants of Sec. 5.2.3 (values of StepArgs::correction).
 constexpr int kCorrVtrace = 0, kCorrNone = 1, kCorrEpsilon = 2, kCorrOneStepIs = 3;
 constexpr int kQBaseline = 1;  // StepArgs::q_estimate: q_s = r_s + gamma_s V(x_{s+1})
@@ -45,6 +33,14 @@ template <typename Args>
 inline bool ratio_needs_fp64(const Args& a) {
   return a.correction == kCorrVtrace && !(a.rho_bar <= 1.0f && a.lambda * a.c_bar <= 1.0f);
 }
+
+// Which row statistics a plain V-trace call takes: the float64 exponent sums
+// (precise mode) whenever it forms loss sums, whose terms over a lane's steps
+// can cancel (Sec. 4.2, App. D: losses summed over batch and time) so that a
+// float32 ratio's rounding moves them by more than the outputs' tolerance, and
+// whenever the weights can amplify ratio errors (ratio_needs_fp64).  Only a
+// targets-only call with every weight at most 1 takes the float32 mode.
+inline bool precise_row_sums(const StepArgs& a, bool losses) { return losses || ratio_needs_fp64(a); }
 
 // The weights a step contributes under a correction variant: rho and c in the
 // value target, and the weight on the advantage.  V-trace uses the truncated

@@ -8,6 +8,7 @@
 // are read straight from global memory; that is simple but not coalesced, which
 // is why the common action counts use the tiled kernel instead.
 #include "device_common.hpp"
+#include "wave_ops.hpp"
 
 namespace vtrace {
 namespace {
@@ -42,33 +43,42 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
       float mz = -INFINITY, my = -INFINITY, za = 0.f, ya = 0.f;
       for (int64_t j = 0; j < A; ++j) {
         const float z = logit_to_float(zr[j]);
-        mz = fmaxf(mz, z);
+        mz = __builtin_elementwise_maximum(mz, z);  // NaN if any logit is NaN
         if (j == act) za = z;
         if (!beh_lp) {
           const float y = logit_to_float(yr[j]);
-          my = fmaxf(my, y);
+          my = __builtin_elementwise_maximum(my, y);
           if (j == act) ya = y;
         }
       }
-      // Exponent sums; also sum_j e_j (z_j - m_z), which gives the entropy as
-      // H = log s - (sum_j e_j (z_j - m_z)) / s.
+      // Exponent sums in float64 (e_j = 2^((l_j - m) log2 e), as the tiled
+      // kernel's precise mode); also sum_j e_j (z_j - m_z) in float32, which
+      // gives the entropy as H = log s - (sum_j e_j (z_j - m_z)) / s.
+      constexpr double kLog2e = 1.4426950408889634;
+      const double mzl = static_cast<double>(mz) * kLog2e;
+      const double myl = static_cast<double>(my) * kLog2e;
       double sz = 0.0, sy = 0.0;
-      float ea = 0.f, ed = 0.f;
+      float ed = 0.f;
       for (int64_t j = 0; j < A; ++j) {
-        const float dz = logit_to_float(zr[j]) - mz;
-        const float e = expf(dz);
-        sz += e;
-        ed += e * dz;
-        if (j == act) ea = e;
-        if (!beh_lp) sy += expf(logit_to_float(yr[j]) - my);
+        const float z = logit_to_float(zr[j]);
+        sz += exp2_f64_term(fma(static_cast<double>(z), kLog2e, -mzl));
+        const float dz = z - mz;
+        ed += expf(dz) * dz;
+        if (!beh_lp) sy += exp2_f64_term(fma(static_cast<double>(logit_to_float(yr[j])), kLog2e, -myl));
       }
+      // A row whose maximum is not finite (NaN or +inf logits) gets NaN sums.
+      if (!__builtin_isfinite(mz)) sz = NAN;
+      if (!beh_lp && !__builtin_isfinite(my)) sy = NAN;
+      const double dza = static_cast<double>(za) - static_cast<double>(mz);  // exact
+      const double ea = exp2_f64_term(fma(static_cast<double>(za), kLog2e, -mzl));
+      const double log_pa_d = dza - log(sz);
 
       // With behaviour log-probabilities the ratio is exp(log pi(a) - log mu(a)).
       const double ratio =
           !valid ? NAN
-          : beh_lp ? exp(static_cast<double>(za) - static_cast<double>(mz) - log(sz) -
-                         static_cast<double>(lmu_g[idx]))
-                   : importance_ratio(za, mz, ya, my, sz, sy);
+          : beh_lp ? exp2_f64((log_pa_d - static_cast<double>(lmu_g[idx])) * kLog2e)
+                   : exp2_f64((dza - (static_cast<double>(ya) - static_cast<double>(my))) * kLog2e) *
+                         (sy / sz);
       if (!valid) raise_error_flag(a.error_flag);
       const StepWeights w = variant_weights(a.correction, clip_above(ratio, rho_bar),
                                             lam * clip_above(ratio, c_bar), lam, valid);
@@ -91,9 +101,9 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
         const float log_s = logf(szf);
         const float H = log_s - ed * inv;
         // 1 - pi(a): the other actions' mass, without cancellation.
-        const float one_minus_pa = static_cast<float>((sz - static_cast<double>(ea)) / sz);
+        const float one_minus_pa = static_cast<float>((sz - ea) / sz);
         // epsilon-correction: -adv log(pi_a + eps) has gradient adv pi_a/(pi_a + eps) (pi_j - 1[j=a]).
-        const float pa = ea * inv;
+        const float pa = static_cast<float>(ea / sz);
         const bool eps_mode = a.correction == kCorrEpsilon;
         const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
         const float adv32 = valid ? static_cast<float>(adv) * pg_w : NAN;
@@ -108,8 +118,8 @@ __global__ __launch_bounds__(kLaneSerialThreads) void lane_serial_kernel(StepArg
             static_cast<float*>(a.d_logits)[idx * A + j] = d;
         }
         const double log_pa = !valid ? NAN
-                              : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
-                                         : static_cast<double>(za - mz) - static_cast<double>(log_s);
+                              : eps_mode ? log(exp(log_pa_d) + static_cast<double>(a.epsilon))
+                                         : log_pa_d;
         acc_pg += -adv * log_pa;
         acc_base += 0.5 * (v_t - V) * (v_t - V);
         acc_ent += -static_cast<double>(H);

@@ -10,6 +10,9 @@ namespace vtrace {
 // Row statistics of one step: what the rest of the step needs from the logits.
 struct RowStats {
   double ratio;       // pi(a|x) / mu(a|x)
+  double log_pa;      // log pi(a|x)
+  double sum, inv;    // s = sum_j exp(z_j - m_z) and 1/s
+  double dza;         // z_a - m_z
   float inv_s;        // 1 / sum_j exp(z_j - m_z)
   float log_s;        // log of that sum
   float H;            // entropy of pi
@@ -18,67 +21,115 @@ struct RowStats {
   float mz;
 };
 
-// kPrecise: the importance ratio feeds products of c over many steps (lambda *
-// c_bar > 1) or is left unclipped above 1 (rho_bar > 1), so errors in it are
-// amplified; the exponent sums are then formed from float64 exponentials of
-// exact float64 differences.  Otherwise every weight is at most 1, nothing is
-// amplified, and float32 exponentials are accurate enough.
+// Maximum of a row of logits, NaN if any logit is NaN (the IEEE maximum,
+// v_maximum3_f32 on gfx950).
+template <int A_, typename In>
+__device__ __forceinline__ float row_max(const In* r) {
+  float m = logit_to_float(r[0]);
+#pragma unroll
+  for (int j = 1; j < A_; ++j) m = __builtin_elementwise_maximum(m, logit_to_float(r[j]));
+  return m;
+}
+
+// kPrecise: the exponent sums, and from them the importance ratio and
+// log pi(a|x), are formed in float64 from float64 exponentials of exact
+// float64 differences (relative error near 1e-10).  Two things need this.  The
+// loss sums over a lane's steps (Sec. 4.2, App. D) can cancel to a few
+// hundredths from a thousand terms of order one, and a float32 ratio (a few
+// 1e-7 relative) then moves them by more than 1e-5; and when the weights can
+// exceed 1 (lambda * c_bar > 1, or rho left unclipped above 1), products of c
+// amplify errors in the ratio.  Otherwise (a targets-only call whose weights
+// are all at most 1) float32 exponentials from the hardware exp2 are accurate
+// enough.  Both modes write the float32 e_j = exp(z_j - m_z) to e[0..A) (the
+// precise mode rounds its float64 ones) for the gradient and the entropy.
+//
+// A row whose maximum is not finite (a NaN or +inf logit, or every logit
+// -inf) gets NaN statistics; -inf logits elsewhere are zero-probability
+// actions.
 //
 // With behaviour log-probabilities (beh_lp) there is no behaviour row: the
 // ratio is exp(log pi(a|x) - lmu), lmu = log mu(a|x) as given.  Variants that
 // do not use the ratio (no_ratio) skip the behaviour row too; their ratio is 1.
-template <int A_, bool kPrecise, typename In>
-__device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
-                                              bool beh_lp, bool no_ratio, float lmu,
-                                              float (&e)[A_]) {
+constexpr double kLog2eF64 = 1.4426950408889634;
+
+// The precise mode's statistics of a target row: everything of RowStats but the
+// ratio.  e_j = 2^((z_j - m_z) log2 e), the fused multiply-add forming the
+// exponent from the exact product z_j log2 e; their float32 roundings go to e.
+template <int A_, typename In>
+__device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, float* e) {
   RowStats st;
   const float za = logit_to_float(zr[act_c]);
-  float mz = logit_to_float(zr[0]);
-#pragma unroll
-  for (int j = 1; j < A_; ++j) mz = fmaxf(mz, logit_to_float(zr[j]));
-  float ya = 0.f, my = 0.f;
-  if (!beh_lp && !no_ratio) {
-    ya = logit_to_float(yr[act_c]);
-    my = logit_to_float(yr[0]);
-#pragma unroll
-    for (int j = 1; j < A_; ++j) my = fmaxf(my, logit_to_float(yr[j]));
-  }
+  const float mz = row_max<A_>(zr);
   st.mz = mz;
+  const double mzl = static_cast<double>(mz) * kLog2eF64;
+  double sz = 0.0;
   float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
-  if constexpr (kPrecise) {
-    // The exponent sums decide the ratio and are formed in float64; a short
-    // unroll keeps their float64 temporaries from crowding out the registers
-    // the rest of the step needs.  The e_j themselves only enter the gradient
-    // and the entropy, where float32 exponentials are accurate enough.
-    double sz = 0.0, sy = 0.0;
 #pragma unroll 3
-    for (int j = 0; j < A_; ++j)
-      sz += exp_nonpos_f64(static_cast<double>(logit_to_float(zr[j])) - static_cast<double>(mz));
-#pragma unroll
-    for (int j = 0; j < A_; ++j) {
-      const float d = logit_to_float(zr[j]) - mz;
-      e[j] = exp_fast(d);
-      ed = fmaf(e[j], d, ed);
-    }
-    const double inv = 1.0 / sz;
-    const double dza = static_cast<double>(za) - static_cast<double>(mz);
-    const double ea = exp_nonpos_f64(dza);
+  for (int j = 0; j < A_; ++j) {
+    const float zj = logit_to_float(zr[j]);
+    const double ej = exp2_f64_term(fma(static_cast<double>(zj), kLog2eF64, -mzl));
+    sz += ej;
+    const float e32 = static_cast<float>(ej);
+    e[j] = e32;
+    ed = fmaf(e32, zj - mz, ed);
+  }
+  if (!__builtin_isfinite(mz)) sz = NAN;
+  const double dza = static_cast<double>(za) - static_cast<double>(mz);  // exact
+  const double ea = exp2_f64_term(fma(static_cast<double>(za), kLog2eF64, -mzl));
+  // 1/s from the hardware reciprocal and two Newton steps.
+  double inv = __builtin_amdgcn_rcp(sz);
+  inv = fma(inv, fma(-sz, inv, 1.0), inv);
+  inv = fma(inv, fma(-sz, inv, 1.0), inv);
+  const double log_sz = log(sz);
+  st.log_pa = dza - log_sz;
+  st.inv_s = static_cast<float>(inv);
+  st.log_s = static_cast<float>(log_sz);
+  st.one_minus_pa = static_cast<float>((sz - ea) * inv);
+  st.e_a = static_cast<float>(ea);
+  st.H = st.log_s - ed * st.inv_s;
+  st.ratio = 0.0;
+  st.sum = sz;
+  st.inv = inv;
+  st.dza = dza;
+  return st;
+}
+
+// Sum of the behaviour row's exponentials in float64 (precise mode), NaN when
+// the row's maximum is not finite; *dya receives y_a - m_y (exact).
+template <int A_, typename In>
+__device__ __forceinline__ double behaviour_exp_sum(const In* yr, int act_c, double* dya) {
+  const float my = row_max<A_>(yr);
+  const double myl = static_cast<double>(my) * kLog2eF64;
+  double sy = 0.0;
+#pragma unroll 3
+  for (int j = 0; j < A_; ++j)
+    sy += exp2_f64_term(fma(static_cast<double>(logit_to_float(yr[j])), kLog2eF64, -myl));
+  if (!__builtin_isfinite(my)) sy = NAN;
+  *dya = static_cast<double>(logit_to_float(yr[act_c])) - static_cast<double>(my);
+  return sy;
+}
+
+template <int A_, bool kPrecise, typename In>
+__device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
+                                              bool beh_lp, bool no_ratio, float lmu, float* e) {
+  if constexpr (kPrecise) {
+    RowStats st = target_row_stats<A_>(zr, act_c, e);
     if (no_ratio) {
       st.ratio = act_ok ? 1.0 : NAN;
     } else if (beh_lp) {
-      st.ratio = act_ok ? exp(dza - log(sz) - static_cast<double>(lmu)) : NAN;
+      st.ratio = act_ok ? exp2_f64((st.log_pa - static_cast<double>(lmu)) * kLog2eF64) : NAN;
     } else {
-#pragma unroll 3
-      for (int j = 0; j < A_; ++j)
-        sy += exp_nonpos_f64(static_cast<double>(logit_to_float(yr[j])) - static_cast<double>(my));
-      const double dya = static_cast<double>(ya) - static_cast<double>(my);
-      st.ratio = act_ok ? exp(dza - dya) * (sy * inv) : NAN;
+      double dya;
+      const double sy = behaviour_exp_sum<A_>(yr, act_c, &dya);
+      st.ratio = act_ok ? exp2_f64((st.dza - dya) * kLog2eF64) * (sy * st.inv) : NAN;
     }
-    st.inv_s = static_cast<float>(inv);
-    st.log_s = static_cast<float>(log(sz));
-    st.one_minus_pa = static_cast<float>((sz - ea) * inv);
-    st.e_a = static_cast<float>(ea);
+    return st;
   } else {
+    RowStats st;
+    const float za = logit_to_float(zr[act_c]);
+    const float mz = row_max<A_>(zr);
+    st.mz = mz;
+    float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
     float sz = 0.f, sy = 0.f;
 #pragma unroll
     for (int j = 0; j < A_; ++j) {
@@ -90,11 +141,14 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
     const float inv = __builtin_amdgcn_rcpf(sz);
     const float ea = exp_fast(za - mz);
     const float log_s = __logf(sz);
+    st.log_pa = static_cast<double>(za - mz) - static_cast<double>(log_s);
     if (no_ratio) {
       st.ratio = act_ok ? 1.0 : NAN;
     } else if (beh_lp) {
       st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - log_s - lmu)) : NAN;
     } else {
+      const float ya = logit_to_float(yr[act_c]);
+      const float my = row_max<A_>(yr);
 #pragma unroll
       for (int j = 0; j < A_; ++j) sy += exp_fast(logit_to_float(yr[j]) - my);
       st.ratio = act_ok ? static_cast<double>(exp_fast((za - mz) - (ya - my)) * (sy * inv)) : NAN;
@@ -103,9 +157,20 @@ __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int ac
     st.log_s = log_s;
     st.one_minus_pa = (sz - ea) * inv;
     st.e_a = ea;
+    st.H = log_s - ed * inv;
+    st.sum = sz;
+    st.inv = inv;
+    st.dza = za - mz;
+    return st;
   }
-  st.H = st.log_s - ed * st.inv_s;
-  return st;
+}
+
+// log(pi(a|x) + eps), the epsilon-correction's policy-gradient log-probability,
+// in the precision of the row statistics.
+template <bool kPrecise>
+__device__ __forceinline__ double log_prob_plus_eps(const RowStats& st, float eps) {
+  if constexpr (kPrecise) return log(exp(st.log_pa) + static_cast<double>(eps));
+  return static_cast<double>(logf(st.e_a * st.inv_s + eps));
 }
 
 }  // namespace vtrace

@@ -48,6 +48,7 @@ namespace {
 
 constexpr int kL = 16;  // default steps per chunk
 
+
 // DPP row_shr:(L-1): lane i of a 16-lane row reads lane i-L+1, so the last
 // lane of every aligned L-lane segment reads the segment's first (L = 16 is
 // kRowShr15).
@@ -264,8 +265,15 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const bool act_ok = act >= 0 && act < A_;
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
-    float e[A_];
-    const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
+    // The gradient kernels take e_j through this thread's row of the gradient
+    // staging tile (free since the previous chunk's stores, which every thread
+    // finished before this chunk's logits barrier), where the gradient row
+    // later replaces them; that keeps them out of the registers through the
+    // recursion.  The targets-only kernels do not use them.
+    static_assert(!kGrad || kPrecise, "loss kernels form their exponent sums in float64");
+    float e_unused[A_];
+    float* const lo = kGrad ? reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_ : e_unused;
+    RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, lo);
     const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
@@ -323,20 +331,14 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
       if (step_ok) {
         a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
-        const double log_pa =
-            !act_ok ? NAN
-            : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
-                       : static_cast<double>(za - st.mz) - static_cast<double>(st.log_s);
+        const double log_pa = !act_ok ? NAN : eps_mode ? log_prob_plus_eps<kPrecise>(st, a.epsilon) : st.log_pa;
         cy.pg += -adv * log_pa;
         cy.base += 0.5 * A_t * A_t;
         cy.ent += -static_cast<double>(st.H);
       }
       float out[A_];
 #pragma unroll
-      for (int j = 0; j < A_; ++j) out[j] = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
-      // The staging tile was last read by the previous chunk's stores, which
-      // every thread finished before this chunk's logits barrier.
-      float* lo = reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_;
+      for (int j = 0; j < A_; ++j) out[j] = lo[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
 #pragma unroll
       for (int j = 0; j < A_; ++j) lo[j] = out[j];
       lo[act_c] = act_ok ? out_a : NAN;
@@ -442,7 +444,7 @@ __device__ __forceinline__ int64_t first_tile_of_workgroup() {
 // The fp64 ratio mode with A > 18 is asked for two waves per SIMD explicitly:
 // left to itself the compiler gives A = 19 two registers more than fit.
 template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kMulti>
-__global__ __launch_bounds__(LANES* L, (kPrecise && A_ > 18) ? 2 : 1) void tiled_kernel(
+__global__ __launch_bounds__(LANES* L, (kPrecise && A_ >= 18) ? 2 : 1) void tiled_kernel(
     StepArgs a, int64_t num_vec_tiles, int64_t tiles_per_wg) {
   using S = Tile<A_, LANES, In, L>;
   constexpr int NT = S::NT;
@@ -589,30 +591,42 @@ int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t 
   return tiles;
 }
 
-// kFastOnly: only the float32 ratio mode is instantiated (the caller has
-// checked ratio_needs_fp64).
+// Loss kernels always take the float64 exponent sums; a targets-only call
+// takes them when its weights can amplify ratio errors.  kFastOnly: only the
+// float32 mode is instantiated (the caller has checked precise_row_sums).
 template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly>
 int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                     bool allow_multi) {
-  if constexpr (!kFastOnly) {
-    if (ratio_needs_fp64(a)) return launch_kernel<A_, LANES, In, L, kGrad, true>(a, st, tiles, vec_tiles, allow_multi);
+  if constexpr (kGrad) {
+    return launch_kernel<A_, LANES, In, L, true, true>(a, st, tiles, vec_tiles, allow_multi);
+  } else {
+    if constexpr (!kFastOnly) {
+      if (precise_row_sums(a, false))
+        return launch_kernel<A_, LANES, In, L, false, true>(a, st, tiles, vec_tiles, allow_multi);
+    }
+    return launch_kernel<A_, LANES, In, L, false, false>(a, st, tiles, vec_tiles, allow_multi);
   }
-  return launch_kernel<A_, LANES, In, L, kGrad, false>(a, st, tiles, vec_tiles, allow_multi);
 }
 
 template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
-  if (kFastOnly && ratio_needs_fp64(a)) return hipErrorInvalidValue;
+  if (kFastOnly && precise_row_sums(a, mode == Mode::LossGrad)) return hipErrorInvalidValue;
+  if constexpr (kFastOnly) {
+    if (mode == Mode::LossGrad) return hipErrorInvalidValue;  // never instantiated
+  }
   const int64_t tiles = (a.B + LANES - 1) / LANES;
   // Vector path: full lane tiles whose time rows start on 16-byte boundaries.
   const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
   const int64_t out_row = a.B * A_ * (a.grad_bf16 ? 2 : 4);
   const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
   const int64_t vec_tiles = aligned ? a.B / LANES : 0;
-  if (mode == Mode::LossGrad)
-    *nwg = launch_mode<A_, LANES, In, L, true, kFastOnly>(a, st, tiles, vec_tiles, allow_multi);
-  else
-    *nwg = launch_mode<A_, LANES, In, L, false, kFastOnly>(a, st, tiles, vec_tiles, allow_multi);
+  if constexpr (!kFastOnly) {
+    if (mode == Mode::LossGrad) {
+      *nwg = launch_mode<A_, LANES, In, L, true, false>(a, st, tiles, vec_tiles, allow_multi);
+      return hipGetLastError();
+    }
+  }
+  *nwg = launch_mode<A_, LANES, In, L, false, kFastOnly>(a, st, tiles, vec_tiles, allow_multi);
   return hipGetLastError();
 }
 
@@ -681,9 +695,8 @@ bool try_shapes(const StepArgs&, Mode, hipStream_t, int64_t*, bool, hipError_t*,
 template <int A_, typename In, typename Sh, typename... Rest>
 bool try_shapes(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi, hipError_t* err,
                 int cus, ShapeTest test) {
-  const bool ok = mode == Mode::LossGrad ? shape_fits<A_, In, true, Sh>(test, a.B, cus)
-                                         : shape_fits<A_, In, false, Sh>(test, a.B, cus);
-  if (ok) {
+  if (mode == Mode::LossGrad) return false;  // the long-run shapes serve targets-only calls
+  if (shape_fits<A_, In, false, Sh>(test, a.B, cus)) {
     *err = launch_shape<A_, Sh::LANES, In, Sh::L, true>(a, mode, st, nwg, allow_multi);
     return true;
   }
@@ -699,7 +712,7 @@ bool try_shapes(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool
 // default shapes measured as fast or faster).
 template <int A_, typename In, typename... Shapes>
 bool launch_long(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi, hipError_t* err) {
-  if (ratio_needs_fp64(a)) return false;
+  if (precise_row_sums(a, mode == Mode::LossGrad)) return false;
   const int cus = compute_units();
   if (cus <= 0) return false;
   return try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::FillsOnce) ||

@@ -64,7 +64,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
   const In* zr = static_cast<const In*>(a.target_logits) + idx * A_;
   const In* yr = static_cast<const In*>(a.behaviour_logits) + idx * A_;
   float e[A_];
-  const RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
+  RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e);
   const double lam = a.lambda;
   const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, static_cast<double>(a.rho_bar)),
                                         lam * clip_above(st.ratio, static_cast<double>(a.c_bar)), lam, act_ok);
@@ -131,10 +131,7 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
     double l_pg = 0.0, l_base = 0.0, l_ent = 0.0;
     if (step_ok) {
       a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
-      const double log_pa =
-          !act_ok ? NAN
-          : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
-                     : static_cast<double>(za - st.mz) - static_cast<double>(st.log_s);
+      const double log_pa = !act_ok ? NAN : eps_mode ? log_prob_plus_eps<kPrecise>(st, a.epsilon) : st.log_pa;
       l_pg = -adv * log_pa;
       l_base = 0.5 * A_t * A_t;
       l_ent = -static_cast<double>(st.H);
@@ -183,14 +180,19 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
   }
 }
 
+// Loss kernels always take the float64 exponent sums (precise_row_sums).
 template <int A_, typename In, bool kGrad>
 void launch_wide_mode(const StepArgs& a, hipStream_t st, unsigned blocks, int tp_log2) {
-  if (ratio_needs_fp64(a))
-    hipLaunchKernelGGL((wide_kernel<A_, In, kGrad, true>), dim3(blocks), dim3(kWideThreads), 0, st, a,
-                       tp_log2);
-  else
-    hipLaunchKernelGGL((wide_kernel<A_, In, kGrad, false>), dim3(blocks), dim3(kWideThreads), 0, st, a,
-                       tp_log2);
+  if constexpr (kGrad) {
+    hipLaunchKernelGGL((wide_kernel<A_, In, true, true>), dim3(blocks), dim3(kWideThreads), 0, st, a, tp_log2);
+  } else {
+    if (precise_row_sums(a, false))
+      hipLaunchKernelGGL((wide_kernel<A_, In, false, true>), dim3(blocks), dim3(kWideThreads), 0, st, a,
+                         tp_log2);
+    else
+      hipLaunchKernelGGL((wide_kernel<A_, In, false, false>), dim3(blocks), dim3(kWideThreads), 0, st, a,
+                         tp_log2);
+  }
 }
 
 template <int A_, typename In>

@@ -12,8 +12,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import (assert_close, assert_sum_close, log_case, loss_term_rss, np_out, oracle_args,
-                      require_gpu, to_device)
+from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
 from synth import PARAM_SETS, make_config, make_random, subset_lanes
 from synth.trajectories import STRESS_SUBSET
 
@@ -40,10 +39,9 @@ def check_against_oracle(tr, p, out, lanes=None):
     assert_close("d_values", pick(np_out(out.d_values)), o.d_values)
     assert_close("d_logits", pick(np_out(out.d_logits)), o.d_logits)
     lane = np_out(out.lane_losses)
-    rss_lane, rss_tot = loss_term_rss(o)
-    assert_sum_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses, rss_lane)
+    assert_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses)
     if lanes is None:
-        assert_sum_close("losses", np_out(out.losses), o.losses, rss_tot)
+        assert_close("losses", np_out(out.losses), o.losses)
     return o
 
 
@@ -99,17 +97,18 @@ def test_stress_subset_matches_oracle(stress, pidx):
 @pytest.mark.parametrize("pidx", [0, 1, 2])
 def test_stress_every_lane_matches_oracle(stress, pidx):
     """The full stress launch (T=1000, B=16384, A=18) with each parameter set
-    ((1, 1, 1) and (1, 0.5, 0.95) take the multi-tile walk, (inf, inf, 1) the
-    fp64 ratio mode), every output element against the oracle, which runs on
-    2048 lanes at a time to bound host memory (lane losses and totals with the
-    sum bound); the totals against the fp64 sum of the oracle's lane losses."""
+    (every one forms its exponent sums in float64), every output element
+    against the oracle, which runs on 2048 lanes at a time to bound host memory;
+    the totals against the fp64 sum of the oracle's lane losses.  Lane losses
+    and totals are held to the element-wise bound: the policy-gradient loss of
+    some lanes is a few hundredths from a thousand terms of order one."""
     tr, dev = stress
     p = PARAM_SETS[4][pidx]
     log_case(f"stress T=1000 B=16384 A=18 {p.label()}, every lane against the oracle")
     out = run_loss_grad(dev, p)
     got = {k: np_out(getattr(out, k)) for k in ("vs", "pg_advantages", "d_values", "d_logits")}
     lane = np_out(out.lane_losses)
-    o_lane, s2 = [], np.zeros(3)
+    o_lane = []
     for l0 in range(0, tr.B, 2048):
         lanes = list(range(l0, min(tr.B, l0 + 2048)))
         o = oracle.loss_and_grads(*oracle_args(subset_lanes(tr, lanes)), p.rho_bar, p.c_bar, p.lam,
@@ -117,12 +116,10 @@ def test_stress_every_lane_matches_oracle(stress, pidx):
         for k, ov in (("vs", o.vs), ("pg_advantages", o.pg_advantages), ("d_values", o.d_values),
                       ("d_logits", o.d_logits)):
             assert_close(f"{k} lanes {l0}..", got[k][:, l0:l0 + len(lanes)], ov)
-        rss_lane, _ = loss_term_rss(o)
-        assert_sum_close(f"lane_losses {l0}..", lane[l0:l0 + len(lanes)], o.lane_losses, rss_lane)
+        assert_close(f"lane_losses {l0}..", lane[l0:l0 + len(lanes)], o.lane_losses)
         o_lane.append(o.lane_losses.astype(np.float64))
-        s2 += (np.asarray(o.step_losses, dtype=np.float64) ** 2).sum(axis=(0, 1))
     tot = np.concatenate(o_lane).sum(axis=0)
-    assert_sum_close("losses", np_out(out.losses)[1:], tot, np.sqrt(s2))
+    assert_close("losses", np_out(out.losses)[1:], tot)
 
 
 EDGE_SHAPES = [
