@@ -84,7 +84,11 @@ typedef enum {
 
 typedef enum {
   VTRACE_F32 = 0,  /* IEEE binary32 logits */
-  VTRACE_BF16 = 1  /* bfloat16 logits (upper half of a binary32) */
+  VTRACE_BF16 = 1, /* bfloat16 logits (upper half of a binary32) */
+  /* Not dtypes: they give the type the range of int32_t, so that any int32
+     value a caller passes is a defined value (rejected with VTRACE_ERR_DTYPE). */
+  VTRACE_DTYPE_RANGE_MIN_ = -0x7fffffff - 1,
+  VTRACE_DTYPE_RANGE_MAX_ = 0x7fffffff
 } vtrace_dtype;
 
 /*
@@ -138,8 +142,12 @@ typedef struct {
 /* Version of this interface; bumped on any incompatible change. */
 int vtrace_abi_version(void);
 
-/* Static, never-NULL description of a status code. */
-const char* vtrace_status_string(vtrace_status s);
+/*
+ * Static, never-NULL description of a status code.  Takes any int32 value (a
+ * vtrace_status converts implicitly); values that are not a vtrace_status give
+ * "unknown status".
+ */
+const char* vtrace_status_string(int32_t status);
 
 /* Largest T*B*A the kernels accept. */
 int64_t vtrace_max_elements(void);

@@ -9,7 +9,10 @@ from __future__ import annotations
 import ctypes
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvtrace.so")
+# VTRACE_LIB names another build of the same library (the host-instrumented
+# one of sanitize.py); by default the in-tree libvtrace.so.
+LIB_PATH = os.environ.get("VTRACE_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                        "libvtrace.so")
 
 VTRACE_F32 = 0
 VTRACE_BF16 = 1
@@ -45,7 +48,7 @@ _F = ctypes.c_float
 _INPUTS = [_I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _P, _P, _P, _P, _F, _F, _F]
 SIGNATURES = {
     "vtrace_abi_version": (ctypes.c_int, []),
-    "vtrace_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "vtrace_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "vtrace_max_elements": (ctypes.c_int64, []),
     "vtrace_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64]),
     "vtrace_workspace_init": (ctypes.c_int, [_P, ctypes.c_size_t, _P]),

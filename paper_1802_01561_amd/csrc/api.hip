@@ -4,7 +4,7 @@
 #include <cstdlib>
 #include <cstring>
 
-#include "../../include/vtrace.h"
+#include "vtrace.h"
 #include "head.hpp"
 #include "launch.hpp"
 
@@ -198,8 +198,8 @@ extern "C" {
 
 int vtrace_abi_version(void) { return kAbiVersion; }
 
-const char* vtrace_status_string(vtrace_status s) {
-  switch (s) {
+const char* vtrace_status_string(int32_t status) {
+  switch (status) {
     case VTRACE_OK: return "ok";
     case VTRACE_ERR_NULL: return "a required pointer is NULL";
     case VTRACE_ERR_SHAPE:
