@@ -7,6 +7,7 @@ the C entry points in include/vtrace.h.
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 from typing import NamedTuple, Optional
 
@@ -38,6 +39,14 @@ def _p(t: Optional[torch.Tensor]):
 def _stream(stream) -> ctypes.c_void_p:
     s = torch.cuda.current_stream() if stream is None else stream
     return ctypes.c_void_p(s.cuda_stream)
+
+
+def _allocating_on(stream):
+    """Allocations made for a call on ``stream`` (workspace, outputs) are made
+    with ``stream`` current, so that torch's caching allocator ties them to the
+    stream the kernels use: a temporary workspace is then not handed out again
+    before the call that uses it has run."""
+    return contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)
 
 
 def _dtype_code(t: torch.Tensor) -> int:
@@ -118,7 +127,8 @@ class Workspace:
         if n == 0:
             raise ValueError(f"invalid batch shape T={T} B={B} A={A} H={H}")
         self.nbytes = n
-        self.tensor = torch.empty(n, dtype=torch.uint8, device=device or "cuda")
+        with _allocating_on(stream):
+            self.tensor = torch.empty(n, dtype=torch.uint8, device=device or "cuda")
         check(lib().vtrace_workspace_init(_p(self.tensor), n, _stream(stream)))
 
     def fits(self, T: int, B: int, A: int, H: Optional[int] = None) -> bool:
@@ -149,10 +159,11 @@ def vtrace_targets(target_logits, behaviour_logits, actions, rewards, discounts,
     variant = _variant(correction, q_estimate, epsilon, behaviour, reward_transform)
     T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
                                  values, bootstrap_value, behaviour)
-    if vs is None:
-        vs = torch.empty((T, B), dtype=torch.float32, device=dev)
-    if pg_advantages is None:
-        pg_advantages = torch.empty((T, B), dtype=torch.float32, device=dev)
+    with _allocating_on(stream):
+        if vs is None:
+            vs = torch.empty((T, B), dtype=torch.float32, device=dev)
+        if pg_advantages is None:
+            pg_advantages = torch.empty((T, B), dtype=torch.float32, device=dev)
     _require(vs, "vs", (T, B), torch.float32, dev)
     _require(pg_advantages, "pg_advantages", (T, B), torch.float32, dev)
     ws, nws = (None, 0) if workspace is None else (_p(workspace.tensor), workspace.nbytes)
@@ -182,12 +193,13 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
         workspace = Workspace(T, B, A, device=dev, stream=stream)
     if out is None:
         f32 = dict(dtype=torch.float32, device=dev)
-        out = LossGrad(
-            torch.empty(4, **f32), torch.empty((T, B, A), dtype=grad_dtype, device=dev),
-            torch.empty((T, B), **f32),
-            torch.empty((T, B), **f32) if with_vs else None,
-            torch.empty((T, B), **f32) if with_pg_advantages else None,
-            torch.empty((B, 3), **f32) if with_lane_losses else None)
+        with _allocating_on(stream):
+            out = LossGrad(
+                torch.empty(4, **f32), torch.empty((T, B, A), dtype=grad_dtype, device=dev),
+                torch.empty((T, B), **f32),
+                torch.empty((T, B), **f32) if with_vs else None,
+                torch.empty((T, B), **f32) if with_pg_advantages else None,
+                torch.empty((B, 3), **f32) if with_lane_losses else None)
     _require(out.losses, "losses", (4,), torch.float32, dev)
     _require(out.d_logits, "d_logits", (T, B, A), grad_dtype, dev)
     _require(out.d_values, "d_values", (T, B), torch.float32, dev)
@@ -256,13 +268,14 @@ def vtrace_head_loss_grad(hidden, head_weight, head_bias, behaviour_logits, acti
         workspace = Workspace(T, B, A, device=dev, stream=stream, H=H)
     if out is None:
         f32 = dict(dtype=torch.float32, device=dev)
-        out = HeadLossGrad(
-            torch.empty(4, **f32), torch.empty((T, B, H), dtype=grad_dtype, device=dev),
-            torch.empty((H, A + 1), **f32), torch.empty(A + 1, **f32),
-            torch.empty((T, B), **f32) if with_vs else None,
-            torch.empty((T, B), **f32) if with_pg_advantages else None,
-            torch.empty((B, 3), **f32) if with_lane_losses else None,
-            torch.empty((T, B, A + 1), **f32) if with_outputs else None)
+        with _allocating_on(stream):
+            out = HeadLossGrad(
+                torch.empty(4, **f32), torch.empty((T, B, H), dtype=grad_dtype, device=dev),
+                torch.empty((H, A + 1), **f32), torch.empty(A + 1, **f32),
+                torch.empty((T, B), **f32) if with_vs else None,
+                torch.empty((T, B), **f32) if with_pg_advantages else None,
+                torch.empty((B, 3), **f32) if with_lane_losses else None,
+                torch.empty((T, B, A + 1), **f32) if with_outputs else None)
     _require(out.losses, "losses", (4,), torch.float32, dev)
     _require(out.d_hidden, "d_hidden", (T, B, H), grad_dtype, dev)
     _require(out.d_weight, "d_weight", (H, A + 1), torch.float32, dev)
@@ -291,7 +304,8 @@ def vtrace_gather_logits(target_logits, behaviour_logits, actions, *, gathered=N
     _require(behaviour_logits, "behaviour_logits", (T, B, A), target_logits.dtype, dev)
     _require(actions, "actions", (T, B), torch.int32, dev)
     if gathered is None:
-        gathered = torch.empty((T, B, 2), dtype=target_logits.dtype, device=dev)
+        with _allocating_on(stream):
+            gathered = torch.empty((T, B, 2), dtype=target_logits.dtype, device=dev)
     _require(gathered, "gathered", (T, B, 2), target_logits.dtype, dev)
     check(lib().vtrace_gather_logits(T, B, A, code, _p(target_logits), _p(behaviour_logits),
                                      _p(actions), _p(gathered), _stream(stream)))
