@@ -4,7 +4,8 @@
  * Weighted Actor-Learner Architectures"), on AMD Instinct MI355X (gfx950).
  *
  * C ABI.  Every array argument is a DEVICE pointer owned by the caller; the
- * library allocates nothing and keeps no global mutable state.  Each call
+ * library allocates nothing and keeps no global mutable state, except the
+ * fixed device array behind vtrace_loss_grad_static.  Each call
  * validates its arguments on the host, enqueues its kernel(s) on `stream`
  * (NULL = the null stream) and returns without synchronising.  A returned
  * VTRACE_OK means the arguments were valid and the launch was accepted; device
@@ -245,6 +246,38 @@ vtrace_status vtrace_loss_grad_ex(
     float* losses, void* d_logits, float* d_values,
     float* vs, float* pg_advantages, float* lane_losses,
     void* workspace, size_t workspace_bytes, vtrace_stream_t stream);
+
+/*
+ * vtrace_loss_grad_ex for callers that cannot allocate device memory: code
+ * being captured into a HIP graph, tight serving loops, harnesses that forbid
+ * hipMalloc.  It takes no workspace and allocates nothing (no hipMalloc,
+ * hipFree or allocating library call): its cross-workgroup loss partials and
+ * completion counter live in a device array of the library,
+ * VTRACE_STATIC_WORKSPACE_BYTES bytes on each device that runs the call, held
+ * until the process ends.  B above VTRACE_STATIC_MAX_LANES gives
+ * VTRACE_ERR_WORKSPACE (use vtrace_loss_grad_ex); every other argument and
+ * error is as in vtrace_loss_grad_ex.
+ *
+ * The first call on a device asks the runtime for the array's address on that
+ * device (the device current at the call) and clears its counter with a fill
+ * kernel on `stream`; later calls on other streams must be ordered after that
+ * first one.  Every call on a device shares the one array: calls that overlap
+ * on a device (concurrent streams, threads) race and give wrong losses, so
+ * order them.  There is no readable error flag: an out-of-range action still
+ * gives NaN outputs as documented above.  Outputs are bit-identical to those
+ * of vtrace_loss_grad_ex on the same inputs.
+ */
+#define VTRACE_STATIC_MAX_LANES 65536
+#define VTRACE_STATIC_WORKSPACE_BYTES (256 + 24 * VTRACE_STATIC_MAX_LANES)
+
+vtrace_status vtrace_loss_grad_static(
+    int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+    const void* target_logits, const void* behaviour_logits, const int32_t* actions,
+    const float* rewards, const float* discounts, const float* values,
+    const float* bootstrap_value, float rho_bar, float c_bar, float lambda,
+    float baseline_cost, float entropy_cost, const vtrace_variant* variant,
+    float* losses, void* d_logits, float* d_values,
+    float* vs, float* pg_advantages, float* lane_losses, vtrace_stream_t stream);
 
 /*
  * Copies of the logits at the taken actions: gathered[t,b,0] = target_logits[t,b,a_t]

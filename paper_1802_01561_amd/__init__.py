@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     vtrace_head_loss_grad,
     vtrace_head_workspace_bytes,
     vtrace_loss_grad,
+    vtrace_loss_grad_static,
     vtrace_max_elements,
     vtrace_targets,
     vtrace_workspace_bytes,

@@ -59,6 +59,8 @@ SIGNATURES = {
                                                    ctypes.c_size_t, _P]),
     "vtrace_loss_grad_ex": (ctypes.c_int, _INPUTS + [_F, _F, ctypes.POINTER(Variant), _P, _P, _P,
                                                      _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "vtrace_loss_grad_static": (ctypes.c_int, _INPUTS + [_F, _F, ctypes.POINTER(Variant), _P, _P, _P, _P,
+                                                         _P, _P, _P]),
     "vtrace_head_workspace_bytes": (ctypes.c_size_t, [_I64, _I64, _I64, _I64]),
     "vtrace_head_loss_grad": (ctypes.c_int, [_I64, _I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _P, _P,
                                              _P, _P, _P, _F, _F, _F, _F, _F,

@@ -26,6 +26,7 @@ __all__ = [
     "vtrace_head_loss_grad",
     "vtrace_head_workspace_bytes",
     "vtrace_loss_grad",
+    "vtrace_loss_grad_static",
     "vtrace_max_elements",
     "vtrace_targets",
     "vtrace_workspace_bytes",
@@ -216,6 +217,44 @@ def vtrace_loss_grad(target_logits, behaviour_logits, actions, rewards, discount
         _p(out.d_values),
         _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses),
         _p(workspace.tensor), workspace.nbytes, _stream(stream)))
+    return out
+
+
+def vtrace_loss_grad_static(target_logits, behaviour_logits, actions, rewards, discounts, values,
+                            bootstrap_value, rho_bar=1.0, c_bar=1.0, lam=1.0, baseline_cost=0.5,
+                            entropy_cost=0.01, *, with_vs=False, with_pg_advantages=False,
+                            with_lane_losses=False, out: Optional[LossGrad] = None, stream=None,
+                            correction="vtrace", q_estimate="vtrace", epsilon=1e-6,
+                            behaviour="logits", reward_transform=None,
+                            grad_dtype=torch.float32) -> LossGrad:
+    """vtrace_loss_grad without a workspace: the library keeps the loss partials
+    in a fixed device array (B <= VTRACE_STATIC_MAX_LANES).  The C call
+    allocates nothing; pass ``out`` to allocate nothing here either.  Calls
+    that overlap on one device race on that array."""
+    variant = _variant(correction, q_estimate, epsilon, behaviour, reward_transform, grad_dtype)
+    T, B, A, code, dev = _inputs(target_logits, behaviour_logits, actions, rewards, discounts,
+                                 values, bootstrap_value, behaviour)
+    if out is None:
+        f32 = dict(dtype=torch.float32, device=dev)
+        with _allocating_on(stream):
+            out = LossGrad(
+                torch.empty(4, **f32), torch.empty((T, B, A), dtype=grad_dtype, device=dev),
+                torch.empty((T, B), **f32),
+                torch.empty((T, B), **f32) if with_vs else None,
+                torch.empty((T, B), **f32) if with_pg_advantages else None,
+                torch.empty((B, 3), **f32) if with_lane_losses else None)
+    _require(out.losses, "losses", (4,), torch.float32, dev)
+    _require(out.d_logits, "d_logits", (T, B, A), grad_dtype, dev)
+    _require(out.d_values, "d_values", (T, B), torch.float32, dev)
+    for name, t, shape in (("vs", out.vs, (T, B)), ("pg_advantages", out.pg_advantages, (T, B)),
+                           ("lane_losses", out.lane_losses, (B, 3))):
+        if t is not None:
+            _require(t, name, shape, torch.float32, dev)
+    check(lib().vtrace_loss_grad_static(
+        T, B, A, code, _p(target_logits), _p(behaviour_logits), _p(actions), _p(rewards),
+        _p(discounts), _p(values), _p(bootstrap_value), rho_bar, c_bar, lam,
+        baseline_cost, entropy_cost, ctypes.byref(variant), _p(out.losses), _p(out.d_logits),
+        _p(out.d_values), _p(out.vs), _p(out.pg_advantages), _p(out.lane_losses), _stream(stream)))
     return out
 
 

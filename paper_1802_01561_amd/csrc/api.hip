@@ -3,6 +3,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "vtrace.h"
 #include "head.hpp"
@@ -192,6 +193,81 @@ vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s)
   return e == hipSuccess ? VTRACE_OK : VTRACE_ERR_HIP;
 }
 
+// Validation and launch arguments of a loss call, except the workspace and
+// the variant.
+vtrace_status loss_grad_args(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype, const void* target_logits,
+                             const void* behaviour_logits, const int32_t* actions, const float* rewards,
+                             const float* discounts, const float* values, const float* bootstrap_value,
+                             float rho_bar, float c_bar, float lambda, float baseline_cost, float entropy_cost,
+                             float* losses, void* d_logits, float* d_values, float* vs, float* pg_advantages,
+                             float* lane_losses, StepArgs* a, LogitsType* lt) {
+  LogitsType lt_local;
+  vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions, rewards,
+                                  discounts, values, bootstrap_value, rho_bar, c_bar, lambda, &lt_local);
+  if (st != VTRACE_OK) return st;
+  if (!std::isfinite(baseline_cost) || !std::isfinite(entropy_cost)) return VTRACE_ERR_PARAM;
+  if (!losses || !d_logits || !d_values) return VTRACE_ERR_NULL;
+  if (!aligned(d_logits, 16)) return VTRACE_ERR_ALIGN;
+  if (!aligned(losses, 4) || !aligned(d_values, 4) || !aligned(vs, 4) || !aligned(pg_advantages, 4) ||
+      !aligned(lane_losses, 4))
+    return VTRACE_ERR_ALIGN;
+  StepArgs args = make_args(T, B, A, target_logits, behaviour_logits, actions, rewards, discounts, values,
+                            bootstrap_value, rho_bar, c_bar, lambda);
+  args.baseline_cost = baseline_cost;
+  args.entropy_cost = entropy_cost;
+  args.losses = losses;
+  args.d_logits = d_logits;
+  args.d_values = d_values;
+  args.vs = vs;
+  args.pg_adv = pg_advantages;
+  args.lane_losses = lane_losses;
+  *a = args;
+  *lt = lt_local;
+  return VTRACE_OK;
+}
+
+// The workspace of vtrace_loss_grad_static: a device array of fixed size,
+// allocated with the library's code object (each device that runs the library
+// holds its own copy until the process ends), so that the call itself
+// allocates nothing.  Layout as a caller's workspace: the 256-byte header
+// (completion counter, error flag) and three float64 partials per workgroup,
+// at most one workgroup per lane.
+constexpr size_t kStaticWorkspaceBytes =
+    vtrace::kWsHeaderBytes + 3 * sizeof(double) * static_cast<size_t>(VTRACE_STATIC_MAX_LANES);
+static_assert(kStaticWorkspaceBytes == VTRACE_STATIC_WORKSPACE_BYTES, "header states the array's size");
+static __device__ __align__(256) unsigned char scratch[kStaticWorkspaceBytes];
+
+// In host code `scratch` names a host-side stand-in, not the device array: the
+// array's address on a device is asked of the runtime once per device, with
+// that device current, and only that address is ever handed to kernels.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_address[kMaxDevices];
+
+// This device's address of `scratch`.  The first call on a device asks for it
+// and clears the array's header with the fill kernel on `s` (the completion
+// counter must start at zero; every loss launch leaves it at zero again).
+vtrace_status static_workspace(hipStream_t s, void** ws) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return VTRACE_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_address[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return VTRACE_ERR_HIP;
+    }
+    (void)hipGetLastError();
+    if (vtrace::launch_fill_zero(p, vtrace::kWsHeaderBytes, s) != hipSuccess) return VTRACE_ERR_HIP;
+    g_scratch_address[dev] = p;
+  }
+  *ws = g_scratch_address[dev];
+  return VTRACE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -303,33 +379,46 @@ vtrace_status vtrace_loss_grad_ex(int64_t T, int64_t B, int64_t A, vtrace_dtype 
                                   float* d_values, float* vs, float* pg_advantages,
                                   float* lane_losses, void* workspace, size_t workspace_bytes,
                                   vtrace_stream_t stream) {
+  StepArgs a;
   LogitsType lt;
-  vtrace_status st = check_common(T, B, A, logits_dtype, target_logits, behaviour_logits, actions,
-                                  rewards, discounts, values, bootstrap_value, rho_bar, c_bar,
-                                  lambda, &lt);
+  vtrace_status st = loss_grad_args(T, B, A, logits_dtype, target_logits, behaviour_logits, actions, rewards,
+                                    discounts, values, bootstrap_value, rho_bar, c_bar, lambda, baseline_cost,
+                                    entropy_cost, losses, d_logits, d_values, vs, pg_advantages, lane_losses, &a,
+                                    &lt);
   if (st != VTRACE_OK) return st;
-  if (!std::isfinite(baseline_cost) || !std::isfinite(entropy_cost)) return VTRACE_ERR_PARAM;
-  if (!losses || !d_logits || !d_values) return VTRACE_ERR_NULL;
-  if (!aligned(d_logits, 16)) return VTRACE_ERR_ALIGN;
-  if (!aligned(losses, 4) || !aligned(d_values, 4) || !aligned(vs, 4) ||
-      !aligned(pg_advantages, 4) || !aligned(lane_losses, 4))
-    return VTRACE_ERR_ALIGN;
   if (!workspace) return VTRACE_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return VTRACE_ERR_ALIGN;
   if (workspace_bytes < workspace_bytes_for(B)) return VTRACE_ERR_WORKSPACE;
-  StepArgs a = make_args(T, B, A, target_logits, behaviour_logits, actions, rewards, discounts,
-                         values, bootstrap_value, rho_bar, c_bar, lambda);
-  a.baseline_cost = baseline_cost;
-  a.entropy_cost = entropy_cost;
-  a.losses = losses;
-  a.d_logits = d_logits;
-  a.d_values = d_values;
-  a.vs = vs;
-  a.pg_adv = pg_advantages;
-  a.lane_losses = lane_losses;
   st = apply_variant(variant, &a);
   if (st != VTRACE_OK) return st;
   attach_workspace(&a, workspace);
+  return launch(a, lt, Mode::LossGrad, as_hip(stream));
+}
+
+vtrace_status vtrace_loss_grad_static(int64_t T, int64_t B, int64_t A, vtrace_dtype logits_dtype,
+                                      const void* target_logits, const void* behaviour_logits,
+                                      const int32_t* actions, const float* rewards,
+                                      const float* discounts, const float* values,
+                                      const float* bootstrap_value, float rho_bar, float c_bar,
+                                      float lambda, float baseline_cost, float entropy_cost,
+                                      const vtrace_variant* variant, float* losses, void* d_logits,
+                                      float* d_values, float* vs, float* pg_advantages,
+                                      float* lane_losses, vtrace_stream_t stream) {
+  StepArgs a;
+  LogitsType lt;
+  vtrace_status st = loss_grad_args(T, B, A, logits_dtype, target_logits, behaviour_logits, actions, rewards,
+                                    discounts, values, bootstrap_value, rho_bar, c_bar, lambda, baseline_cost,
+                                    entropy_cost, losses, d_logits, d_values, vs, pg_advantages, lane_losses, &a,
+                                    &lt);
+  if (st != VTRACE_OK) return st;
+  if (B > VTRACE_STATIC_MAX_LANES) return VTRACE_ERR_WORKSPACE;
+  st = apply_variant(variant, &a);
+  if (st != VTRACE_OK) return st;
+  void* ws = nullptr;
+  st = static_workspace(as_hip(stream), &ws);
+  if (st != VTRACE_OK) return st;
+  attach_workspace(&a, ws);
+  a.error_flag = nullptr;  // nothing reads a flag in the shared array
   return launch(a, lt, Mode::LossGrad, as_hip(stream));
 }
 

@@ -34,7 +34,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(_lib.SIGNATURES)
@@ -275,3 +275,31 @@ def test_python_head_binding_validates_before_calling():
         v.vtrace_head_loss_grad(*args, correction="retrace")
     with pytest.raises(ValueError):
         v.vtrace_head_loss_grad(*args, grad_dtype=torch.float16)
+
+
+def test_static_loss_grad_rejects_before_any_device_call(L):
+    """vtrace_loss_grad_static validates like vtrace_loss_grad_ex and refuses
+    batches wider than its fixed device array; every call here fails before
+    the library asks for that array."""
+    V = _lib.Variant
+    base = dict(T=5, B=4, A=9, dt=0, tl=P, bl=P, act=P, r=P, d=P, v=P, boot=P, rho=1.0, c=1.0,
+                lam=1.0, cv=0.5, ce=0.01, losses=P, dl=P, dv=P, variant=None)
+
+    def st(**kw):
+        a = dict(base)
+        a.update(kw)
+        return L.vtrace_loss_grad_static(a["T"], a["B"], a["A"], a["dt"], a["tl"], a["bl"],
+                                         a["act"], a["r"], a["d"], a["v"], a["boot"], a["rho"],
+                                         a["c"], a["lam"], a["cv"], a["ce"], a["variant"],
+                                         a["losses"], a["dl"], a["dv"], None, None, None, None)
+
+    assert st(B=65537) == WS
+    assert st(B=1 << 20, T=1, A=2) == WS
+    assert st(T=0) == SHAPE
+    assert st(losses=None) == NULL
+    assert st(dl=P + 4) == ALIGN
+    assert st(dt=7) == DTYPE
+    assert st(lam=1.5) == PARAM
+    assert st(cv=math.nan) == PARAM
+    assert st(variant=ctypes.byref(V(9, 0, 1e-6))) == PARAM
+    assert st(B=65537, variant=ctypes.byref(V(9, 0, 1e-6))) == WS
