@@ -20,6 +20,21 @@ __device__ __forceinline__ float logit_to_float(uint16_t bits) {
 // ratio stays NaN (fmin would return `bar`).  min(+inf, x) = x.
 __device__ __forceinline__ double clip_above(double x, double bar) { return x > bar ? bar : x; }
 
+// p + n elements (or bytes) for an n that may put the result before the array:
+// a chunk's row 0 lies before t = 0 in a lane's last chunk, where only rows
+// from t = 0 on are accessed.  Integer arithmetic, so that no out-of-range
+// pointer is formed.
+template <typename T>
+__device__ __forceinline__ T* offset_elems(T* p, int64_t n) {
+  return reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(n * int64_t(sizeof(T))));
+}
+__device__ __forceinline__ const char* offset_bytes(const void* p, int64_t bytes) {
+  return reinterpret_cast<const char*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes));
+}
+__device__ __forceinline__ char* offset_bytes(void* p, int64_t bytes) {
+  return reinterpret_cast<char*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes));
+}
+
 // Correction variants of Sec. 5.2.3 (values of StepArgs::correction).
 constexpr int kCorrVtrace = 0, kCorrNone = 1, kCorrEpsilon = 2, kCorrOneStepIs = 3;
 constexpr int kQBaseline = 1;  // StepArgs::q_estimate: q_s = r_s + gamma_s V(x_{s+1})

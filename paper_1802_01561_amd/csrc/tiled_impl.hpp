@@ -131,6 +131,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
   const int64_t out_row = B * A_ * gsz;
   const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
+  auto lane_ok_of = [&](int64_t b0) { return kMulti || b0 + lane_local < B; };  // the walk takes full tiles
 
   // Register prefetch (vector path): NV 16-byte vectors covering both tensors,
   // plus this thread's action, reward, discount and value, and at a tile's
@@ -139,38 +140,46 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   int32_t p_act = 0;
   float p_r = 0.f, p_g = 0.f, p_V = 0.f, p_lmu = 0.f, p_boot = 0.f;
 
+  // Vector-path addresses are a wave-uniform base (the chunk's row 0 at the
+  // tile's first lane, in scalar registers) plus a per-thread 32-bit offset,
+  // the form of the loads' and stores' scalar-base addressing; the launcher
+  // takes the vector path only where L rows of every array fit 32-bit offsets.
+  const uint32_t in_row32 = static_cast<uint32_t>(in_row);
+  const uint32_t out_row32 = static_cast<uint32_t>(out_row);
+  const uint32_t B32 = static_cast<uint32_t>(B);
   auto prefetch = [&](int64_t tile, int k) {
     const int64_t b0 = tile * LANES;
-    const int64_t b = b0 + lane_local;
-    const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
-    const char* const zg = static_cast<const char*>(a.target_logits) + b0 * A_ * int64_t(sizeof(In));
-    const char* const yg = static_cast<const char*>(a.behaviour_logits) + b0 * A_ * int64_t(sizeof(In));
     const int64_t t0 = T - static_cast<int64_t>(k + 1) * L;
-    const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row 0
+    const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row `neg`
+    const int64_t row0 = t0 * B + b0;                     // may be negative: only rows >= neg are read
+    const char* const zg = offset_bytes(a.target_logits, row0 * A_ * int64_t(sizeof(In)));
+    const char* const yg = offset_bytes(a.behaviour_logits, row0 * A_ * int64_t(sizeof(In)));
     static_for<S::NV>([&](auto I) {
       constexpr int i = decltype(I)::value;
+      // Which tensor vector i of every thread belongs to, where that is known
+      // at compile time (all but the vector that straddles the two tiles).
+      constexpr bool kAllZ = (i + 1) * NT <= S::IN_TILE16;
+      constexpr bool kAllY = i * NT >= S::IN_TILE16;
+      constexpr bool kTail = i * NT + NT > 2 * S::IN_TILE16;
       const int f = tid + i * NT;
-      const bool is_y = f >= S::IN_TILE16;
-      if ((i * NT + NT <= 2 * S::IN_TILE16 || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
+      const bool is_y = kAllY || (!kAllZ && f >= S::IN_TILE16);
+      if ((!kTail || f < 2 * S::IN_TILE16) && !(is_y && skip_y)) {
         const int g = is_y ? f - S::IN_TILE16 : f;
         int r = g / S::IN_ROW16;
         const int c = g % S::IN_ROW16;
         r = r < neg ? neg : r;
-        const char* base = is_y ? yg : zg;
-        pre[i] = __builtin_nontemporal_load(
-            reinterpret_cast<const v4u*>(base + (t0 + r) * in_row + c * 16));
+        const uint32_t off = static_cast<uint32_t>(r) * in_row32 + static_cast<uint32_t>(c) * 16u;
+        pre[i] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>((is_y ? yg : zg) + off));
       }
     });
-    int64_t t = t0 + s;
-    t = t < 0 ? 0 : t;
-    if (lane_ok) {
-      const int64_t idx = t * B + b;
-      p_act = a.actions[idx];
-      p_r = a.rewards[idx];
-      p_g = a.discounts[idx];
-      p_V = a.values[idx];
-      if (beh_lp && !no_ratio) p_lmu = lmu_g[idx];
-      if (kMulti && k == 0) p_boot = a.bootstrap_value[b];
+    if (lane_ok_of(b0)) {
+      const uint32_t off = static_cast<uint32_t>(s < neg ? neg : s) * B32 + static_cast<uint32_t>(lane_local);
+      p_act = offset_elems(a.actions, row0)[off];
+      p_r = offset_elems(a.rewards, row0)[off];
+      p_g = offset_elems(a.discounts, row0)[off];
+      p_V = offset_elems(a.values, row0)[off];
+      if (beh_lp && !no_ratio) p_lmu = offset_elems(lmu_g, row0)[off];
+      if (kMulti && k == 0) p_boot = a.bootstrap_value[b0 + lane_local];
     }
   };
 
@@ -188,7 +197,6 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const int64_t b = b0 + lane_local;
     const bool lane_ok = kMulti || b < B;  // the multi-tile walk takes full tiles only
     const int nb = static_cast<int>(B - b0 < LANES ? B - b0 : LANES);
-    char* const dg = static_cast<char*>(a.d_logits) + b0 * A_ * gsz;
     if constexpr (kMulti) {
       if (k == 0) {
         // A new tile: the carry past its last step is the bootstrap value
@@ -201,6 +209,10 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const int64_t t = t0 + s;
     const bool step_ok = lane_ok && t >= 0;
     const int64_t idx = t * B + b;
+    // [T,B] element (t, b) as the chunk's uniform row 0 plus a 32-bit offset
+    // (vector path); where step_ok, t >= 0.
+    const int64_t row0 = t0 * B + b0;
+    const uint32_t soff = static_cast<uint32_t>(s) * B32 + static_cast<uint32_t>(lane_local);
 
     // Every thread is past the previous chunk's row reads: the gradient
     // kernels passed their staging barrier after them; the targets-only
@@ -311,8 +323,13 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     cy.V = dpp_f64<row_shr_to_last<L>()>(V);
 
     if (step_ok) {
-      if (a.vs) a.vs[idx] = static_cast<float>(v_t);
-      if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+      if constexpr (kVec) {
+        if (a.vs) offset_elems(a.vs, row0)[soff] = static_cast<float>(v_t);
+        if (a.pg_adv) offset_elems(a.pg_adv, row0)[soff] = static_cast<float>(adv);
+      } else {
+        if (a.vs) a.vs[idx] = static_cast<float>(v_t);
+        if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+      }
     }
 
     if constexpr (kGrad) {
@@ -330,7 +347,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       const float za = logit_to_float(zr[act_c]);
       const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
       if (step_ok) {
-        a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+        const float dv = static_cast<float>(a.baseline_cost * (V - v_t));
+        if constexpr (kVec)
+          offset_elems(a.d_values, row0)[soff] = dv;
+        else
+          a.d_values[idx] = dv;
         const double log_pa = !act_ok ? NAN : eps_mode ? log_prob_plus_eps<kPrecise>(st, a.epsilon) : st.log_pa;
         cy.pg += -adv * log_pa;
         cy.base += 0.5 * A_t * A_t;
@@ -345,6 +366,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       __syncthreads();
       if constexpr (kVec) {
         const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
+        char* const dgr = offset_bytes(a.d_logits, row0 * A_ * gsz);  // the chunk's row 0
         if (!grad_bf16) {
           static_for<S::NO>([&](auto I) {
             constexpr int i = decltype(I)::value;
@@ -354,7 +376,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
               if (rr >= neg)
                 __builtin_nontemporal_store(
                     lds_g[rr * S::OUT_PITCH16 + cc],
-                    reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+                    reinterpret_cast<v4u*>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
+                                                  static_cast<uint32_t>(cc) * 16u)));
             }
           });
         } else {
@@ -370,8 +393,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
               pk.y = pack_bf16x2(__uint_as_float(lo.z), __uint_as_float(lo.w));
               pk.z = pack_bf16x2(__uint_as_float(hi.x), __uint_as_float(hi.y));
               pk.w = pack_bf16x2(__uint_as_float(hi.z), __uint_as_float(hi.w));
-              __builtin_nontemporal_store(pk,
-                                          reinterpret_cast<v4u*>(dg + (t0 + rr) * out_row + cc * 16));
+              __builtin_nontemporal_store(pk, reinterpret_cast<v4u*>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
+                                                                             static_cast<uint32_t>(cc) * 16u)));
             }
           }
         }
@@ -619,7 +642,11 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
   const int64_t in_row = a.B * A_ * int64_t(sizeof(In));
   const int64_t out_row = a.B * A_ * (a.grad_bf16 ? 2 : 4);
   const bool aligned = (in_row % 16 == 0) && (out_row % 16 == 0);
-  const int64_t vec_tiles = aligned ? a.B / LANES : 0;
+  // The vector path addresses L rows of each array from a uniform base with
+  // 32-bit offsets (L rows of logits, of gradients, of [T,B] scalars).
+  constexpr int64_t k4G = int64_t(1) << 32;
+  const bool offsets32 = L * in_row < k4G && L * out_row < k4G && L * a.B * 4 < k4G;
+  const int64_t vec_tiles = aligned && offsets32 ? a.B / LANES : 0;
   if constexpr (!kFastOnly) {
     if (mode == Mode::LossGrad) {
       *nwg = launch_mode<A_, LANES, In, L, true, false>(a, st, tiles, vec_tiles, allow_multi);
