@@ -1,14 +1,12 @@
 """Helpers for the GPU tests: device upload of synthetic batches and the parity
 checks used throughout.
 
-Element-wise outputs meet |g - o| <= 1e-5 + 1e-4 |o|.  Outputs that are sums of
-many terms (a lane's loss over its steps, the loss totals over the batch) are
-held to |g - o| <= 1e-5 + 1e-4 |o| + 1e-4 RSS, RSS the root-sum-square of the
-terms: each term within 1e-4 of itself gives, for independent errors, an
-error of about 1e-4 RSS in the sum.  When the terms cancel (a policy-gradient
-loss of a few hundredths from a thousand terms of order one) that is far more
-than 1e-4 of the total: the float32 log-probability in each term alone
-contributes about 1e-7 of it per step."""
+Every output is held element by element to |g - o| <= 1e-5 + 1e-4 |o|.  The
+fused output-layer call's sums alone (its lane and total losses, d_W, d_b and
+each d_hidden element) add a term kappa * RSS, RSS the root-sum-square of the
+sum's terms and kappa the relative precision its terms are formed with
+(``head_kappa_*``: the layer's float32 outputs, its bfloat16 high/low split of
+dL/do and its float32 accumulation of d_W and d_b)."""
 
 from __future__ import annotations
 
@@ -68,13 +66,44 @@ def assert_close(name, got, expect, rtol=RTOL, atol=ATOL):
             f"worst at {worst}: got {got[worst]!r} expected {expect[worst]!r}")
 
 
-def assert_sum_close(name, got, expect, rss, rtol=RTOL, atol=ATOL):
-    """The sum bound above, |got - expect| <= atol + rtol (|expect| + rss)."""
+U32 = 2.0 ** -24  # float32 unit roundoff
+G_SPLIT = 2.0 ** -17  # dL/do as a bfloat16 high and low pair: relative precision
+
+
+def head_kappa_loss(H: int) -> float:
+    """Relative precision of a loss term of the output-layer call: the layer's
+    outputs are H-term bfloat16 dot products accumulated in float32, within
+    about 2^-24 sqrt(H) of themselves, and the step's softmax statistics are
+    float32 (a few roundings, 8 allowed)."""
+    return U32 * (float(np.sqrt(H)) + 8.0)
+
+
+def head_kappa_hidden(H: int) -> float:
+    """Of a term G[c] W[k, c] of d_hidden: dL/do enters the product as a
+    bfloat16 high and low pair (2^-17), computed from outputs within
+    2^-24 sqrt(H)."""
+    return G_SPLIT + U32 * float(np.sqrt(H))
+
+
+def head_kappa_param(H: int, T: int, B: int) -> float:
+    """Of a term of d_W or d_b: as for d_hidden, and the workgroup accumulates
+    its terms in float32 over all its steps and lanes (about 2^-24 sqrt(n) for
+    n of them: T steps of the 4-lane groups it walks, at most 512 workgroups)
+    before the workgroups' partials are added in float64."""
+    quads = -(-B // 4)
+    nwg = min(quads, 512)
+    n = T * 4 * (-(-quads // nwg))
+    return G_SPLIT + U32 * (float(np.sqrt(H)) + float(np.sqrt(n)))
+
+
+def assert_sum_close(name, got, expect, rss, kappa, rtol=RTOL, atol=ATOL):
+    """|got - expect| <= atol + rtol |expect| + kappa rss: the element-wise bound
+    plus kappa times the root-sum-square of the sum's terms."""
     got = np.asarray(got, dtype=np.float64)
     expect = np.asarray(expect, dtype=np.float64)
     assert got.shape == expect.shape, (name, got.shape, expect.shape)
     err = np.abs(got - expect)
-    bound = atol + rtol * np.abs(expect) + rtol * np.asarray(rss, dtype=np.float64)
+    bound = atol + rtol * np.abs(expect) + kappa * np.asarray(rss, dtype=np.float64)
     bad = ~(err <= bound)
     if bad.any():
         ratio = np.where(np.isfinite(err), err / bound, np.inf)

@@ -21,7 +21,8 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import ATOL, RTOL, assert_close, assert_sum_close, log_case, np_out, require_gpu
+from gpu_util import (ATOL, RTOL, assert_close, assert_sum_close, head_kappa_hidden, head_kappa_loss,
+                      head_kappa_param, log_case, np_out, require_gpu)
 from synth import HEAD_WORKLOADS, Params, make_head, make_head_config, subset_head_lanes
 
 pytestmark = pytest.mark.gpu
@@ -77,24 +78,25 @@ def check_head(hb, p, out, *, behaviour_values=None, grad_bf16=False, lanes=None
     assert_close("outputs", pick(np_out(out.outputs)), o.outputs)
     assert_close("vs", pick(np_out(out.vs)), o.vs)
     assert_close("pg_advantages", pick(np_out(out.pg_advantages)), o.pg_advantages)
+    kl, kh = head_kappa_loss(sub.H), head_kappa_hidden(sub.H)
     lane = np_out(out.lane_losses)
     rss_lane = np.sqrt((o.step_losses ** 2).sum(axis=0))
-    assert_sum_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses, rss_lane)
+    assert_sum_close("lane_losses", lane if lanes is None else lane[lanes], o.lane_losses, rss_lane, kl)
     W = sub.weight.astype(np.float64)
     rss_h = np.sqrt((o.d_outputs ** 2) @ (W.T ** 2))
     dh = pick(np_out(out.d_hidden))
     if grad_bf16:
-        err_ok = np.abs(dh - o.d_hidden) <= BF16_ATOL + BF16_RTOL * np.abs(o.d_hidden) + RTOL * rss_h
-        assert err_ok.all(), f"d_hidden (bf16): {int((~err_ok).sum())} elements outside the bound"
+        assert_sum_close("d_hidden (bf16)", dh, o.d_hidden, rss_h, kh, rtol=BF16_RTOL, atol=BF16_ATOL)
     else:
-        assert_sum_close("d_hidden", dh, o.d_hidden, rss_h)
+        assert_sum_close("d_hidden", dh, o.d_hidden, rss_h, kh)
     if lanes is None and whole:
         rss_w, rss_b = oracle.sum_term_scale(sub.hidden, o.d_outputs)
-        assert_sum_close("d_weight", np_out(out.d_weight), o.d_weight, rss_w)
-        assert_sum_close("d_bias", np_out(out.d_bias), o.d_bias, rss_b)
+        kp = head_kappa_param(sub.H, sub.T, sub.B)
+        assert_sum_close("d_weight", np_out(out.d_weight), o.d_weight, rss_w, kp)
+        assert_sum_close("d_bias", np_out(out.d_bias), o.d_bias, rss_b, kp)
         s2 = (o.step_losses ** 2).sum(axis=(0, 1))
         rss_tot = np.sqrt(np.concatenate([[s2.sum()], s2]))
-        assert_sum_close("losses", np_out(out.losses), o.losses, rss_tot)
+        assert_sum_close("losses", np_out(out.losses), o.losses, rss_tot, kl)
     return o
 
 
@@ -233,8 +235,8 @@ def test_head_matches_plain_kernel_on_its_outputs():
 def test_head_stress_every_lane():
     """The full stress shape with (1, 1, 1): every per-step and per-lane output
     against the oracle, 512 lanes at a time, and d_W, d_b and the loss totals
-    against the oracle's sums over all chunks (the sum bound, with the RSS of
-    all their terms)."""
+    against the oracle's sums over all chunks (the sum bound, kappa times the
+    RSS of all their terms)."""
     from synth import SEED_BASE, head_batch_from_device, make_head_device
     c = HEAD_WORKLOADS["stress"]
     log_case("head stress, every lane: generating on the device")
@@ -262,10 +264,11 @@ def test_head_stress_every_lane():
         rw, rb = oracle.sum_term_scale(hb.hidden, o.d_outputs)
         dw += o.d_weight; db += o.d_bias; tot += o.losses[1:]
         rw2 += rw ** 2; rb2 += rb ** 2; s2 += (o.step_losses ** 2).sum(axis=(0, 1))
-    assert_sum_close("d_weight", np_out(out.d_weight), dw, np.sqrt(rw2))
-    assert_sum_close("d_bias", np_out(out.d_bias), db, np.sqrt(rb2))
-    assert_sum_close("losses", np_out(out.losses),
-                     np.concatenate([[tot.sum()], tot]), np.sqrt(np.concatenate([[s2.sum()], s2])))
+    kp = head_kappa_param(c["H"], c["T"], c["B"])
+    assert_sum_close("d_weight", np_out(out.d_weight), dw, np.sqrt(rw2), kp)
+    assert_sum_close("d_bias", np_out(out.d_bias), db, np.sqrt(rb2), kp)
+    assert_sum_close("losses", np_out(out.losses), np.concatenate([[tot.sum()], tot]),
+                     np.sqrt(np.concatenate([[s2.sum()], s2])), head_kappa_loss(c["H"]))
     del out, d, dev
     torch.cuda.empty_cache()
 
