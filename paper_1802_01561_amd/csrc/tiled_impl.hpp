@@ -104,7 +104,7 @@ struct Carry {
 // tile_stride, i < ntiles, one after another as one loop over their chunks, so
 // that the prefetch runs across tile boundaries; each lane's loss totals are
 // then added to acc[3 * lane], a slot only the lane's step-0 thread touches.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kVec, bool kMulti>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kVec, bool kMulti, bool kPlain>
 __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t first_tile,
                                            int64_t tile_stride, int64_t ntiles, Carry& cy,
                                            double* acc) {
@@ -123,11 +123,17 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
 
   // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
-  const bool beh_lp = a.behaviour_log_probs != 0;
+  // kPlain: the call is plain V-trace (logits of both policies, rewards as
+  // given, q_s from v_{s+1}, float32 gradients), so every variant switch below
+  // is a compile-time constant.
+  const int correction = kPlain ? kCorrVtrace : a.correction;
+  const int q_estimate = kPlain ? 0 : a.q_estimate;
+  const int reward_transform = kPlain ? 0 : a.reward_transform;
+  const bool beh_lp = !kPlain && a.behaviour_log_probs != 0;
   // No-correction and epsilon-correction never look at the behaviour policy.
-  const bool no_ratio = a.correction == kCorrNone || a.correction == kCorrEpsilon;
+  const bool no_ratio = correction == kCorrNone || correction == kCorrEpsilon;
   const bool skip_y = beh_lp || no_ratio;
-  const bool grad_bf16 = a.grad_bf16 != 0;
+  const bool grad_bf16 = !kPlain && a.grad_bf16 != 0;
   const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
   const int64_t out_row = B * A_ * gsz;
   const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
@@ -268,7 +274,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       }
       __syncthreads();
     }
-    r32 = transform_reward(r32, a.reward_transform);
+    r32 = transform_reward(r32, reward_transform);
     if (!step_ok) act = 0;  // rows that do not exist carry a harmless action
 
     // This thread's rows.
@@ -286,7 +292,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     float e_unused[A_];
     float* const lo = kGrad ? reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_ : e_unused;
     RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, lo);
-    const StepWeights w = variant_weights(a.correction, clip_above(st.ratio, rho_bar),
+    const StepWeights w = variant_weights(correction, clip_above(st.ratio, rho_bar),
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
     const double r = r32, g = g32, V = V32;
@@ -313,7 +319,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const double v_t = V + A_t;
     double v_next = dpp_f64<kRowShl1>(v_t);
     if (s == L - 1) v_next = cy.v;
-    const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
+    const double q_next = q_estimate == kQBaseline ? V_next : v_next;
     const double adv = w.rho_pg * (r + g * q_next - V);
 
     // The segment's first step becomes the carry of the earlier chunk, held by
@@ -339,7 +345,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       // epsilon-correction: the policy-gradient term is -adv log(pi_a + eps),
       // whose gradient is adv pi_a/(pi_a + eps) (pi_j - 1[j=a]).
       const float pa = st.e_a * st.inv_s;
-      const bool eps_mode = a.correction == kCorrEpsilon;
+      const bool eps_mode = correction == kCorrEpsilon;
       const float pg_w = eps_mode ? pa / (pa + a.epsilon) : 1.0f;
       const float adv32 = static_cast<float>(adv) * pg_w;
       const float beta = st.inv_s * ce;
@@ -466,7 +472,7 @@ __device__ __forceinline__ int64_t first_tile_of_workgroup() {
 // workgroups whenever a slot frees, and leave the chip partly idle at the end.
 // The fp64 ratio mode with A > 18 is asked for two waves per SIMD explicitly:
 // left to itself the compiler gives A = 19 two registers more than fit.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kMulti>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kMulti, bool kPlain = false>
 __global__ __launch_bounds__(LANES* L, (kPrecise && A_ >= 18) ? 2 : 1) void tiled_kernel(
     StepArgs a, int64_t num_vec_tiles, int64_t tiles_per_wg) {
   using S = Tile<A_, LANES, In, L>;
@@ -481,7 +487,7 @@ __global__ __launch_bounds__(LANES* L, (kPrecise && A_ >= 18) ? 2 : 1) void tile
     __shared__ double acc[3 * LANES];  // per-lane loss sums over the workgroup's tiles
     if (s == 0) acc[3 * lane_local + 0] = acc[3 * lane_local + 1] = acc[3 * lane_local + 2] = 0.0;
     Carry cy{0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-    chunk_walk<A_, LANES, In, L, kGrad, kPrecise, true, true>(a, lds, first_tile_of_workgroup<LANES>(),
+    chunk_walk<A_, LANES, In, L, kGrad, kPrecise, true, true, kPlain>(a, lds, first_tile_of_workgroup<LANES>(),
                                                               gridDim.x, tiles_per_wg, cy, acc);
     if constexpr (kGrad) {
       double pg = 0.0, base = 0.0, ent = 0.0;
@@ -500,9 +506,9 @@ __global__ __launch_bounds__(LANES* L, (kPrecise && A_ >= 18) ? 2 : 1) void tile
     Carry cy{boot, boot, 0.0, 0.0, 0.0, 0.0};
 
     if (tile < num_vec_tiles)
-      chunk_walk<A_, LANES, In, L, kGrad, kPrecise, true, false>(a, lds, tile, 0, 1, cy, nullptr);
+      chunk_walk<A_, LANES, In, L, kGrad, kPrecise, true, false, kPlain>(a, lds, tile, 0, 1, cy, nullptr);
     else
-      chunk_walk<A_, LANES, In, L, kGrad, kPrecise, false, false>(a, lds, tile, 0, 1, cy, nullptr);
+      chunk_walk<A_, LANES, In, L, kGrad, kPrecise, false, false, kPlain>(a, lds, tile, 0, 1, cy, nullptr);
 
     if constexpr (kGrad) {
       // Per-lane totals over the row (fixed butterfly order), then the workgroup.
@@ -595,7 +601,7 @@ int compute_units() {
 // the longer walk, and with one resident workgroup per CU (the 512-thread
 // kernel of bfloat16 logits with A = 18) the multi-tile walk measured 4-10%
 // slower.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kPlain = false>
 int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                       bool allow_multi) {
   if constexpr (!kPrecise) {
@@ -609,8 +615,8 @@ int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t 
       }
     }
   }
-  hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, L, kGrad, kPrecise, false>), dim3(static_cast<unsigned>(tiles)),
-                     dim3(LANES * L), 0, st, a, vec_tiles, int64_t(1));
+  hipLaunchKernelGGL((tiled_kernel<A_, LANES, In, L, kGrad, kPrecise, false, kPlain>),
+                     dim3(static_cast<unsigned>(tiles)), dim3(LANES * L), 0, st, a, vec_tiles, int64_t(1));
   return tiles;
 }
 
@@ -621,6 +627,7 @@ template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly>
 int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                     bool allow_multi) {
   if constexpr (kGrad) {
+    if (is_plain_vtrace(a)) return launch_kernel<A_, LANES, In, L, true, true, true>(a, st, tiles, vec_tiles, allow_multi);
     return launch_kernel<A_, LANES, In, L, true, true>(a, st, tiles, vec_tiles, allow_multi);
   } else {
     if constexpr (!kFastOnly) {
