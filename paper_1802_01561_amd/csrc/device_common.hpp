@@ -20,19 +20,27 @@ __device__ __forceinline__ float logit_to_float(uint16_t bits) {
 // ratio stays NaN (fmin would return `bar`).  min(+inf, x) = x.
 __device__ __forceinline__ double clip_above(double x, double bar) { return x > bar ? bar : x; }
 
+// Pointers into global memory.  An access through a generic pointer is a flat
+// instruction, which the hardware also counts as an LDS operation, so every
+// wait for an LDS read would wait for the loads in flight as well.
+template <typename T>
+using gptr = __attribute__((address_space(1))) T*;
+
 // p + n elements (or bytes) for an n that may put the result before the array:
 // a chunk's row 0 lies before t = 0 in a lane's last chunk, where only rows
 // from t = 0 on are accessed.  Integer arithmetic, so that no out-of-range
-// pointer is formed.
+// pointer is formed; the result is a global pointer (see gptr).
 template <typename T>
-__device__ __forceinline__ T* offset_elems(T* p, int64_t n) {
-  return reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(n * int64_t(sizeof(T))));
+__device__ __forceinline__ gptr<T> offset_elems(T* p, int64_t n) {
+  return (gptr<T>)(reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(p) +
+                                        static_cast<uintptr_t>(n * int64_t(sizeof(T)))));
 }
-__device__ __forceinline__ const char* offset_bytes(const void* p, int64_t bytes) {
-  return reinterpret_cast<const char*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes));
+__device__ __forceinline__ gptr<const char> offset_bytes(const void* p, int64_t bytes) {
+  return (gptr<const char>)(reinterpret_cast<const char*>(reinterpret_cast<uintptr_t>(p) +
+                                                          static_cast<uintptr_t>(bytes)));
 }
-__device__ __forceinline__ char* offset_bytes(void* p, int64_t bytes) {
-  return reinterpret_cast<char*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes));
+__device__ __forceinline__ gptr<char> offset_bytes(void* p, int64_t bytes) {
+  return (gptr<char>)(reinterpret_cast<char*>(reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes)));
 }
 
 // Correction variants of Sec. 5.2.3 (values of StepArgs::correction).

@@ -158,8 +158,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const int64_t t0 = T - static_cast<int64_t>(k + 1) * L;
     const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;  // rows before t = 0 reread row `neg`
     const int64_t row0 = t0 * B + b0;                     // may be negative: only rows >= neg are read
-    const char* const zg = offset_bytes(a.target_logits, row0 * A_ * int64_t(sizeof(In)));
-    const char* const yg = offset_bytes(a.behaviour_logits, row0 * A_ * int64_t(sizeof(In)));
+    const gptr<const char> zg = offset_bytes(a.target_logits, row0 * A_ * int64_t(sizeof(In)));
+    const gptr<const char> yg = offset_bytes(a.behaviour_logits, row0 * A_ * int64_t(sizeof(In)));
     static_for<S::NV>([&](auto I) {
       constexpr int i = decltype(I)::value;
       // Which tensor vector i of every thread belongs to, where that is known
@@ -175,7 +175,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         const int c = g % S::IN_ROW16;
         r = r < neg ? neg : r;
         const uint32_t off = static_cast<uint32_t>(r) * in_row32 + static_cast<uint32_t>(c) * 16u;
-        pre[i] = __builtin_nontemporal_load(reinterpret_cast<const v4u*>((is_y ? yg : zg) + off));
+        pre[i] = __builtin_nontemporal_load(reinterpret_cast<gptr<const v4u>>((is_y ? yg : zg) + off));
       }
     });
     if (lane_ok_of(b0)) {
@@ -372,7 +372,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       __syncthreads();
       if constexpr (kVec) {
         const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
-        char* const dgr = offset_bytes(a.d_logits, row0 * A_ * gsz);  // the chunk's row 0
+        const gptr<char> dgr = offset_bytes(a.d_logits, row0 * A_ * gsz);  // the chunk's row 0
         if (!grad_bf16) {
           static_for<S::NO>([&](auto I) {
             constexpr int i = decltype(I)::value;
@@ -382,7 +382,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
               if (rr >= neg)
                 __builtin_nontemporal_store(
                     lds_g[rr * S::OUT_PITCH16 + cc],
-                    reinterpret_cast<v4u*>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
+                    reinterpret_cast<gptr<v4u>>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
                                                   static_cast<uint32_t>(cc) * 16u)));
             }
           });
@@ -399,7 +399,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
               pk.y = pack_bf16x2(__uint_as_float(lo.z), __uint_as_float(lo.w));
               pk.z = pack_bf16x2(__uint_as_float(hi.x), __uint_as_float(hi.y));
               pk.w = pack_bf16x2(__uint_as_float(hi.z), __uint_as_float(hi.w));
-              __builtin_nontemporal_store(pk, reinterpret_cast<v4u*>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
+              __builtin_nontemporal_store(pk, reinterpret_cast<gptr<v4u>>(dgr + (static_cast<uint32_t>(rr) * out_row32 +
                                                                              static_cast<uint32_t>(cc) * 16u)));
             }
           }
