@@ -51,6 +51,7 @@ __device__ __forceinline__ float row_max(const In* r) {
 // ratio is exp(log pi(a|x) - lmu), lmu = log mu(a|x) as given.  Variants that
 // do not use the ratio (no_ratio) skip the behaviour row too; their ratio is 1.
 constexpr double kLog2eF64 = 1.4426950408889634;
+constexpr double kLn2F64 = 0.6931471805599453;
 
 // The precise mode's statistics of a target row: everything of RowStats but the
 // ratio.  e_j = 2^((z_j - m_z) log2 e), the fused multiply-add forming the
@@ -63,15 +64,14 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
   st.mz = mz;
   const double mzl = static_cast<double>(mz) * kLog2eF64;
   double sz = 0.0;
-  float ed = 0.f;  // sum_j e_j (z_j - m_z), for the entropy
+  double ed = 0.0;  // sum_j e_j (z_j - m_z) log2 e, for the entropy
 #pragma unroll 3
   for (int j = 0; j < A_; ++j) {
-    const float zj = logit_to_float(zr[j]);
-    const double ej = exp2_f64_term(fma(static_cast<double>(zj), kLog2eF64, -mzl));
+    const double xj = fma(static_cast<double>(logit_to_float(zr[j])), kLog2eF64, -mzl);
+    const double ej = exp2_f64_term(xj);
     sz += ej;
-    const float e32 = static_cast<float>(ej);
-    e[j] = e32;
-    ed = fmaf(e32, zj - mz, ed);
+    e[j] = static_cast<float>(ej);
+    ed = fma(ej, xj, ed);
   }
   if (!__builtin_isfinite(mz)) sz = NAN;
   const double dza = static_cast<double>(za) - static_cast<double>(mz);  // exact
@@ -86,7 +86,7 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
   st.log_s = static_cast<float>(log_sz);
   st.one_minus_pa = static_cast<float>((sz - ea) * inv);
   st.e_a = static_cast<float>(ea);
-  st.H = st.log_s - ed * st.inv_s;
+  st.H = static_cast<float>(fma(-ed * kLn2F64, inv, log_sz));
   st.ratio = 0.0;
   st.sum = sz;
   st.inv = inv;

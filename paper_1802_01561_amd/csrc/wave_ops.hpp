@@ -73,24 +73,38 @@ __device__ __forceinline__ double exp_nonpos_f64(double x) {
 }
 
 // 2^x in float64 for |x| <= 1100 (the caller bounds x).  x = k + f with k the
-// nearest integer and |f| <= 1/2; 2^f is a degree-7 polynomial, the
-// interpolant of 2^f at the eight Chebyshev nodes of [-1/2, 1/2] (relative
-// error below 6e-11 over the interval); the result is scaled by 2^k.  k is
-// formed by adding 1.5 * 2^52, which leaves the nearest integer to x in the
-// low word of the sum (no float-to-integer conversion; NaN gives NaN).
+// nearest integer and |f| <= 1/2; 2^f is the polynomial of degree kDegree that
+// interpolates 2^f at the kDegree + 1 Chebyshev nodes of [-1/2, 1/2] (relative
+// error below 6e-11 over the interval for degree 7, below 2.6e-9 for degree
+// 6); the result is scaled by 2^k.  k is formed by adding 1.5 * 2^52, which
+// leaves the nearest integer to x in the low word of the sum (no
+// float-to-integer conversion; NaN gives NaN).
+template <int kDegree = 7>
 __device__ __forceinline__ double exp2_f64_bounded(double x) {
+  static_assert(kDegree == 6 || kDegree == 7, "degree 6 or 7");
   constexpr double kRound = 6755399441055744.0;  // 1.5 * 2^52
   const double t = x + kRound;
   const int k = static_cast<int>(static_cast<unsigned>(__double_as_longlong(t) & 0xffffffffu));
   const double f = x - (t - kRound);
-  double p = 1.5303701161442145e-05;
-  p = fma(p, f, 1.5469729221575116e-04);
-  p = fma(p, f, 1.3333478471058548e-03);
-  p = fma(p, f, 9.6180256132689674e-03);
-  p = fma(p, f, 5.5504109063307244e-02);
-  p = fma(p, f, 2.4022651213498578e-01);
-  p = fma(p, f, 6.9314718055682956e-01);
-  p = fma(p, f, 9.9999999995956212e-01);
+  double p;
+  if constexpr (kDegree == 7) {
+    p = 1.5303701161442145e-05;
+    p = fma(p, f, 1.5469729221575116e-04);
+    p = fma(p, f, 1.3333478471058548e-03);
+    p = fma(p, f, 9.6180256132689674e-03);
+    p = fma(p, f, 5.5504109063307244e-02);
+    p = fma(p, f, 2.4022651213498578e-01);
+    p = fma(p, f, 6.9314718055682956e-01);
+    p = fma(p, f, 9.9999999995956212e-01);
+  } else {
+    p = 1.5461444698569130e-04;
+    p = fma(p, f, 1.3400428177615838e-03);
+    p = fma(p, f, 9.6180566785246370e-03);
+    p = fma(p, f, 5.5503272266703020e-02);
+    p = fma(p, f, 2.4022650922288757e-01);
+    p = fma(p, f, 6.9314720670283260e-01);
+    p = fma(p, f, 1.0);
+  }
   return __builtin_ldexp(p, k);
 }
 
@@ -103,12 +117,14 @@ __device__ __forceinline__ double exp2_f64(double x) {
   return exp2_f64_bounded(x);
 }
 
-// 2^x for a term of an exponent sum, x <= 0 up to rounding: arguments below
-// -1100 (-inf included) are raised by the hardware maximum, one instruction,
-// which also turns NaN into a term of 0.  Callers find rows with NaN logits
+// 2^x for a term of an exponent sum, x <= 0 up to rounding, from the degree-6
+// polynomial (a sum of such terms is within 2.6e-9 of itself, twenty times
+// below a float32 rounding): arguments below -1100 (-inf included) are raised
+// by the hardware maximum, one instruction, which also turns NaN into a term
+// of 0.  Callers find rows with NaN logits
 // from the row's maximum instead (row_max propagates NaN).
 __device__ __forceinline__ double exp2_f64_term(double x) {
-  return exp2_f64_bounded(__builtin_fmax(x, -1100.0));
+  return exp2_f64_bounded<6>(__builtin_fmax(x, -1100.0));
 }
 
 // Workgroups are handed to the 8 XCDs round-robin; number the lane tiles so
