@@ -56,23 +56,40 @@ constexpr double kLn2F64 = 0.6931471805599453;
 // The precise mode's statistics of a target row: everything of RowStats but the
 // ratio.  e_j = 2^((z_j - m_z) log2 e), the fused multiply-add forming the
 // exponent from the exact product z_j log2 e; their float32 roundings go to e.
+// The precise mode reads a row once into registers (one batch of LDS reads and
+// one wait) and forms its terms fully unrolled.  An empty asm statement after
+// each term pins the running sums in place: otherwise the compiler sinks the
+// additions below all A_ exponentials and keeps every term live, more
+// registers than two waves per SIMD have.
+template <int A_, typename In>
+__device__ __forceinline__ float read_row_max(const In* r, float (&v)[A_]) {
+#pragma unroll
+  for (int j = 0; j < A_; ++j) v[j] = logit_to_float(r[j]);
+  float m = v[0];
+#pragma unroll
+  for (int j = 1; j < A_; ++j) m = __builtin_elementwise_maximum(m, v[j]);
+  return m;
+}
+
 template <int A_, typename In>
 __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, float* e) {
   RowStats st;
   const float za = logit_to_float(zr[act_c]);
-  const float mz = row_max<A_>(zr);
+  float z[A_];
+  const float mz = read_row_max<A_>(zr, z);
   st.mz = mz;
   const double mzl = static_cast<double>(mz) * kLog2eF64;
   double sz = 0.0;
   double ed = 0.0;  // sum_j e_j (z_j - m_z) log2 e, for the entropy
-#pragma unroll 3
-  for (int j = 0; j < A_; ++j) {
-    const double xj = fma(static_cast<double>(logit_to_float(zr[j])), kLog2eF64, -mzl);
+  static_for<A_>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    const double xj = fma(static_cast<double>(z[j]), kLog2eF64, -mzl);
     const double ej = exp2_f64_term(xj);
     sz += ej;
     e[j] = static_cast<float>(ej);
     ed = fma(ej, xj, ed);
-  }
+    asm volatile("" : "+v"(sz), "+v"(ed));
+  });
   if (!__builtin_isfinite(mz)) sz = NAN;
   const double dza = static_cast<double>(za) - static_cast<double>(mz);  // exact
   const double ea = exp2_f64_term(fma(static_cast<double>(za), kLog2eF64, -mzl));
@@ -98,12 +115,15 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
 // the row's maximum is not finite; *dya receives y_a - m_y (exact).
 template <int A_, typename In>
 __device__ __forceinline__ double behaviour_exp_sum(const In* yr, int act_c, double* dya) {
-  const float my = row_max<A_>(yr);
+  float y[A_];
+  const float my = read_row_max<A_>(yr, y);
   const double myl = static_cast<double>(my) * kLog2eF64;
   double sy = 0.0;
-#pragma unroll 3
-  for (int j = 0; j < A_; ++j)
-    sy += exp2_f64_term(fma(static_cast<double>(logit_to_float(yr[j])), kLog2eF64, -myl));
+  static_for<A_>([&](auto J) {
+    constexpr int j = decltype(J)::value;
+    sy += exp2_f64_term(fma(static_cast<double>(y[j]), kLog2eF64, -myl));
+    asm volatile("" : "+v"(sy));
+  });
   if (!__builtin_isfinite(my)) sy = NAN;
   *dya = static_cast<double>(logit_to_float(yr[act_c])) - static_cast<double>(my);
   return sy;

@@ -23,7 +23,8 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // DPP row moves on a double (two 32-bit halves).  Lanes whose source falls
-// outside their row of 16 keep their own value.
+// outside their row of 16 read 0 (bound_ctrl), so the move needs no copy of
+// the old value; every caller overrides or ignores those lanes.
 //   0x100 + k (row_shl:k): lane i of a row reads lane i+k;
 //   kRowShr15 (row_shr:15): lane 15 of a row reads lane 0.
 template <int kCtrl>
@@ -31,8 +32,8 @@ __device__ __forceinline__ double dpp_f64(double x) {
   const unsigned long long u = __double_as_longlong(x);
   int lo = static_cast<int>(u & 0xffffffffu);
   int hi = static_cast<int>(u >> 32);
-  lo = __builtin_amdgcn_update_dpp(lo, lo, kCtrl, 0xF, 0xF, false);
-  hi = __builtin_amdgcn_update_dpp(hi, hi, kCtrl, 0xF, 0xF, false);
+  lo = __builtin_amdgcn_update_dpp(0, lo, kCtrl, 0xF, 0xF, true);
+  hi = __builtin_amdgcn_update_dpp(0, hi, kCtrl, 0xF, 0xF, true);
   return __longlong_as_double(static_cast<long long>(
       (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
 }
