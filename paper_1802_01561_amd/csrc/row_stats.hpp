@@ -72,11 +72,15 @@ __device__ __forceinline__ float read_row_max(const In* r, float (&v)[A_]) {
 }
 
 template <int A_, typename In>
-__device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, float* e) {
+__device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, float* e, float* zo) {
   RowStats st;
   const float za = logit_to_float(zr[act_c]);
   float z[A_];
   const float mz = read_row_max<A_>(zr, z);
+  if (zo != nullptr) {
+#pragma unroll
+    for (int j = 0; j < A_; ++j) zo[j] = z[j];
+  }
   st.mz = mz;
   const double mzl = static_cast<double>(mz) * kLog2eF64;
   double sz = 0.0;
@@ -129,11 +133,15 @@ __device__ __forceinline__ double behaviour_exp_sum(const In* yr, int act_c, dou
   return sy;
 }
 
+//
+// zo (precise mode; may be null) receives the target row as float32, for
+// callers that keep it in registers until the gradient.
 template <int A_, bool kPrecise, typename In>
 __device__ __forceinline__ RowStats row_stats(const In* zr, const In* yr, int act_c, bool act_ok,
-                                              bool beh_lp, bool no_ratio, float lmu, float* e) {
+                                              bool beh_lp, bool no_ratio, float lmu, float* e,
+                                              float* zo = nullptr) {
   if constexpr (kPrecise) {
-    RowStats st = target_row_stats<A_>(zr, act_c, e);
+    RowStats st = target_row_stats<A_>(zr, act_c, e, zo);
     if (no_ratio) {
       st.ratio = act_ok ? 1.0 : NAN;
     } else if (beh_lp) {

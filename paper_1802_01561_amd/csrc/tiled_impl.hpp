@@ -283,15 +283,22 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const bool act_ok = act >= 0 && act < A_;
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
-    // The gradient kernels take e_j through this thread's row of the gradient
-    // staging tile (free since the previous chunk's stores, which every thread
-    // finished before this chunk's logits barrier), where the gradient row
-    // later replaces them; that keeps them out of the registers through the
-    // recursion.  The targets-only kernels do not use them.
+    // e_j and z_j for the gradient.  The plain loss kernels keep both in
+    // registers from the row statistics to the gradient (36 VGPRs that their
+    // two waves per SIMD have), which spares each row two LDS round trips;
+    // the variant kernels, which need those registers for their switches,
+    // take e_j through this thread's row of the gradient staging tile (free
+    // since the previous chunk's stores, which every thread finished before
+    // this chunk's logits barrier), where the gradient row later replaces
+    // them, and read z_j again from the logit tile.  The targets-only kernels
+    // use neither.
     static_assert(!kGrad || kPrecise, "loss kernels form their exponent sums in float64");
-    float e_unused[A_];
-    float* const lo = kGrad ? reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_ : e_unused;
-    RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, lo);
+    constexpr bool kRowRegs = kGrad && kPlain;
+    float* const lo = reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_;
+    float e_reg[A_], z_reg[A_];
+    float* const e_out = kGrad && !kRowRegs ? lo : e_reg;
+    RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e_out,
+                                          kRowRegs ? z_reg : nullptr);
     const StepWeights w = variant_weights(correction, clip_above(st.ratio, rho_bar),
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
@@ -365,7 +372,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       }
       float out[A_];
 #pragma unroll
-      for (int j = 0; j < A_; ++j) out[j] = lo[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
+      for (int j = 0; j < A_; ++j) out[j] = e_out[j] * fmaf(beta, kRowRegs ? z_reg[j] : logit_to_float(zr[j]), alpha);
 #pragma unroll
       for (int j = 0; j < A_; ++j) lo[j] = out[j];
       lo[act_c] = act_ok ? out_a : NAN;
@@ -729,7 +736,7 @@ bool try_shapes(const StepArgs&, Mode, hipStream_t, int64_t*, bool, hipError_t*,
 template <int A_, typename In, typename Sh, typename... Rest>
 bool try_shapes(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi, hipError_t* err,
                 int cus, ShapeTest test) {
-  if (mode == Mode::LossGrad) return false;  // the long-run shapes serve targets-only calls
+  if (mode == Mode::LossGrad) return false;  // loss calls: launch_long_loss
   if (shape_fits<A_, In, false, Sh>(test, a.B, cus)) {
     *err = launch_shape<A_, Sh::LANES, In, Sh::L, true>(a, mode, st, nwg, allow_multi);
     return true;
@@ -752,6 +759,57 @@ bool launch_long(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, boo
   return try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::FillsOnce) ||
          try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::WalksEvenly) ||
          try_shapes<A_, In, Shapes...>(a, mode, st, nwg, allow_multi, err, cus, ShapeTest::WholeGenerations);
+}
+
+// Workgroups of the single-tile loss kernel (plain or with variants) that fit
+// on a compute unit at once, asked of the runtime once (0 if it cannot say).
+template <int A_, int LANES, typename In, int L, bool kPlain>
+int loss_workgroups_per_cu() {
+  static std::atomic<int> cached{-1};
+  int n = cached.load(std::memory_order_relaxed);
+  if (n < 0) {
+    int blocks = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &blocks, reinterpret_cast<const void*>(tiled_kernel<A_, LANES, In, L, true, true, false, kPlain>),
+            LANES * L, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      blocks = 0;
+    }
+    n = blocks > 0 ? blocks : 0;
+    cached.store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+// Loss calls on the long-run shapes: the first of Shapes whose workgroups run
+// the batch as 1 to kMaxGenerations whole generations of resident workgroups,
+// each CU holding at least kMinWavesPerCu waves; false (launching nothing)
+// when none applies.  (The loss kernels fit two workgroups of 256 threads per
+// CU, so the multi-tile walk, which needs more, does not serve them.)
+template <int A_, typename In>
+bool launch_long_loss(const StepArgs&, hipStream_t, int64_t*, hipError_t*, int) {
+  return false;
+}
+template <int A_, typename In, typename Sh, typename... Rest>
+bool launch_long_loss(const StepArgs& a, hipStream_t st, int64_t* nwg, hipError_t* err, int cus) {
+  if (a.B % Sh::LANES == 0) {
+    const int64_t tiles = a.B / Sh::LANES;
+    const int per_cu = is_plain_vtrace(a) ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, true>()
+                                          : loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, false>();
+    const int64_t resident = static_cast<int64_t>(per_cu) * cus;
+    if (per_cu * (Sh::LANES * Sh::L / kWave) >= kMinWavesPerCu && resident > 0 && tiles % resident == 0 &&
+        tiles <= kMaxGenerations * resident) {
+      *err = launch_shape<A_, Sh::LANES, In, Sh::L>(a, Mode::LossGrad, st, nwg, false);
+      return true;
+    }
+  }
+  return launch_long_loss<A_, In, Rest...>(a, st, nwg, err, cus);
+}
+template <int A_, typename In, typename... Shapes>
+bool launch_long_loss(const StepArgs& a, hipStream_t st, int64_t* nwg, hipError_t* err) {
+  const int cus = compute_units();
+  if (cus <= 0) return false;
+  return launch_long_loss<A_, In, Shapes...>(a, st, nwg, err, cus);
 }
 
 // Launch for action count A with 16 lanes per workgroup, fp32 or bf16 logits.

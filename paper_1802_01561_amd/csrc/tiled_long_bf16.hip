@@ -10,6 +10,8 @@ namespace vtrace {
 
 bool launch_tiled_long_bf16(const StepArgs& a, Mode mode, hipStream_t st, int64_t* num_workgroups,
                             bool allow_multi, hipError_t* err) {
+  // Loss calls with A = 18: 32 lanes x 8 steps (2304-byte runs per time row).
+  if (mode == Mode::LossGrad) return a.A == 18 && launch_long_loss<18, uint16_t, Shape<32, 8>>(a, st, num_workgroups, err);
   if (a.A == 18)
     return launch_long<18, uint16_t, Shape<128, 4>, Shape<64, 8>, Shape<64, 4>>(a, mode, st, num_workgroups,
                                                                                allow_multi, err);
