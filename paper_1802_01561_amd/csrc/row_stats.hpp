@@ -83,8 +83,10 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
   }
   st.mz = mz;
   const double mzl = static_cast<double>(mz) * kLog2eF64;
-  double sz = 0.0;
-  double ed = 0.0;  // sum_j e_j (z_j - m_z) log2 e, for the entropy
+  // The sums start from -0.0, the additive identity, which lets the compiler
+  // drop the first addition.
+  double sz = -0.0;
+  double ed = -0.0;  // sum_j e_j (z_j - m_z) log2 e, for the entropy
   static_for<A_>([&](auto J) {
     constexpr int j = decltype(J)::value;
     const double xj = fma(static_cast<double>(z[j]), kLog2eF64, -mzl);
@@ -101,7 +103,7 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
   double inv = __builtin_amdgcn_rcp(sz);
   inv = fma(inv, fma(-sz, inv, 1.0), inv);
   inv = fma(inv, fma(-sz, inv, 1.0), inv);
-  const double log_sz = log(sz);
+  const double log_sz = log_sum_f64(sz);
   st.log_pa = dza - log_sz;
   st.inv_s = static_cast<float>(inv);
   st.log_s = static_cast<float>(log_sz);
@@ -122,7 +124,7 @@ __device__ __forceinline__ double behaviour_exp_sum(const In* yr, int act_c, dou
   float y[A_];
   const float my = read_row_max<A_>(yr, y);
   const double myl = static_cast<double>(my) * kLog2eF64;
-  double sy = 0.0;
+  double sy = -0.0;
   static_for<A_>([&](auto J) {
     constexpr int j = decltype(J)::value;
     sy += exp2_f64_term(fma(static_cast<double>(y[j]), kLog2eF64, -myl));

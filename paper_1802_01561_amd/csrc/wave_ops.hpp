@@ -128,6 +128,19 @@ __device__ __forceinline__ double exp2_f64_term(double x) {
   return exp2_f64_bounded<6>(__builtin_fmax(x, -1100.0));
 }
 
+// log s in float64 for an exponent sum s in [1, 2^64) (a sum whose largest
+// term is 1): the hardware float32 base-2 logarithm as the start, l = log2 s
+// to about 1e-7, then one Newton step for f(y) = e^y - s from y0 = l ln2,
+// y1 = y0 - 1 + s e^{-y0} with e^{-y0} = 2^{-l} from the degree-7 exponential:
+// the step squares the start's error, so what remains is that exponential's
+// relative error (below 6e-11) and a few float64 roundings.  NaN stays NaN.
+__device__ __forceinline__ double log_sum_f64(double s) {
+  constexpr double kLn2 = 0.6931471805599453;
+  const double l = static_cast<double>(__builtin_amdgcn_logf(static_cast<float>(s)));
+  const double y0 = l * kLn2;
+  return fma(s, exp2_f64_bounded<7>(-l), y0 - 1.0);
+}
+
 // Workgroups are handed to the 8 XCDs round-robin; number the lane tiles so
 // that neighbouring tiles (which share 128-byte lines of the [T,B] arrays) run
 // on the same XCD and meet in its L2.
