@@ -2,6 +2,8 @@
 // tiled and time-parallel V-trace kernels.
 #pragma once
 
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "wave_ops.hpp"
 
@@ -71,6 +73,18 @@ __device__ __forceinline__ float read_row_max(const In* r, float (&v)[A_]) {
   return m;
 }
 
+// Whether every row of the wave is finite (its maximum m and its minimum
+// both finite): then no exponent-sum term needs the clamp against -inf and
+// NaN logits, and the whole wave takes the unclamped terms (36 VALU
+// instructions fewer per step for 9 to find the minimum).
+template <int A_>
+__device__ __forceinline__ bool wave_rows_finite(const float (&v)[A_], float m) {
+  float mn = v[0];
+#pragma unroll
+  for (int j = 1; j < A_; ++j) mn = __builtin_elementwise_minimum(mn, v[j]);
+  return __all(__builtin_isfinite(mn) && __builtin_isfinite(m)) != 0;
+}
+
 template <int A_, typename In>
 __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, float* e, float* zo) {
   RowStats st;
@@ -87,18 +101,26 @@ __device__ __forceinline__ RowStats target_row_stats(const In* zr, int act_c, fl
   // drop the first addition.
   double sz = -0.0;
   double ed = -0.0;  // sum_j e_j (z_j - m_z) log2 e, for the entropy
-  static_for<A_>([&](auto J) {
-    constexpr int j = decltype(J)::value;
-    const double xj = fma(static_cast<double>(z[j]), kLog2eF64, -mzl);
-    const double ej = exp2_f64_term(xj);
-    sz += ej;
-    e[j] = static_cast<float>(ej);
-    ed = fma(ej, xj, ed);
-    asm volatile("" : "+v"(sz), "+v"(ed));
-  });
+  double ea;
+  auto terms = [&](auto clamp) {
+    constexpr bool kClamp = decltype(clamp)::value;
+    static_for<A_>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      const double xj = fma(static_cast<double>(z[j]), kLog2eF64, -mzl);
+      const double ej = exp2_f64_term<kClamp>(xj);
+      sz += ej;
+      e[j] = static_cast<float>(ej);
+      ed = fma(ej, xj, ed);
+      asm volatile("" : "+v"(sz), "+v"(ed));
+    });
+    ea = exp2_f64_term<kClamp>(fma(static_cast<double>(za), kLog2eF64, -mzl));
+  };
+  if (wave_rows_finite<A_>(z, mz))
+    terms(std::false_type{});
+  else
+    terms(std::true_type{});
   if (!__builtin_isfinite(mz)) sz = NAN;
   const double dza = static_cast<double>(za) - static_cast<double>(mz);  // exact
-  const double ea = exp2_f64_term(fma(static_cast<double>(za), kLog2eF64, -mzl));
   // 1/s from the hardware reciprocal and two Newton steps.
   double inv = __builtin_amdgcn_rcp(sz);
   inv = fma(inv, fma(-sz, inv, 1.0), inv);
@@ -125,11 +147,18 @@ __device__ __forceinline__ double behaviour_exp_sum(const In* yr, int act_c, dou
   const float my = read_row_max<A_>(yr, y);
   const double myl = static_cast<double>(my) * kLog2eF64;
   double sy = -0.0;
-  static_for<A_>([&](auto J) {
-    constexpr int j = decltype(J)::value;
-    sy += exp2_f64_term(fma(static_cast<double>(y[j]), kLog2eF64, -myl));
-    asm volatile("" : "+v"(sy));
-  });
+  auto terms = [&](auto clamp) {
+    constexpr bool kClamp = decltype(clamp)::value;
+    static_for<A_>([&](auto J) {
+      constexpr int j = decltype(J)::value;
+      sy += exp2_f64_term<kClamp>(fma(static_cast<double>(y[j]), kLog2eF64, -myl));
+      asm volatile("" : "+v"(sy));
+    });
+  };
+  if (wave_rows_finite<A_>(y, my))
+    terms(std::false_type{});
+  else
+    terms(std::true_type{});
   if (!__builtin_isfinite(my)) sy = NAN;
   *dya = static_cast<double>(logit_to_float(yr[act_c])) - static_cast<double>(my);
   return sy;

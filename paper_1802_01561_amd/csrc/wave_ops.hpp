@@ -124,8 +124,13 @@ __device__ __forceinline__ double exp2_f64(double x) {
 // by the hardware maximum, one instruction, which also turns NaN into a term
 // of 0.  Callers find rows with NaN logits
 // from the row's maximum instead (row_max propagates NaN).
+// kClamp false: for callers that know x is finite (a term of a row whose
+// logits are all finite), where no clamp is needed: a finite x below -1100
+// gives 2^k p(f) with k below -1100, which underflows to 0 all the same.
+template <bool kClamp = true>
 __device__ __forceinline__ double exp2_f64_term(double x) {
-  return exp2_f64_bounded<6>(__builtin_fmax(x, -1100.0));
+  if constexpr (kClamp) return exp2_f64_bounded<6>(__builtin_fmax(x, -1100.0));
+  return exp2_f64_bounded<6>(x);
 }
 
 // log s in float64 for an exponent sum s in [1, 2^64) (a sum whose largest

@@ -209,6 +209,35 @@ def test_out_of_range_actions_give_nan_and_flag():
     assert vt.vtrace_error_flag(ws2) == 0
 
 
+@pytest.mark.parametrize("T,B,A", [(40, 64, 18), (1000, 16384, 18), (100, 4096, 9)])
+def test_nonfinite_logit_rows_leave_the_other_lanes_exact(T, B, A):
+    """A NaN target logit in one lane's row and a NaN behaviour logit in
+    another's.  Those rows' statistics are NaN (so are the recursion's values
+    at and before them, and the two lanes' losses), and every wave holding
+    such a row forms its exponent sums with the terms clamped against
+    non-finite logits; the other lanes of those waves, and all other lanes,
+    still match the oracle element by element (shapes: 16-step tiles, the
+    32 x 8 loss tiles of the stress batch, A = 9)."""
+    tr = make_random(T, B, A, 1234, noise_std=1.0)
+    bz, tz, by, ty = 5, T // 2, B - 3, T // 3
+    tr.target_logits[tz, bz, 3] = np.nan
+    tr.behaviour_logits[ty, by, A - 2] = np.nan
+    p = PARAM_SETS[4][0]
+    log_case(f"non-finite logits T={T} B={B} A={A}")
+    out = run_loss_grad(to_device(tr), p)
+    lane = np_out(out.lane_losses)
+    assert np.isnan(lane[bz, 0]) and np.isnan(lane[by, 0])
+    vs = np_out(out.vs)
+    assert np.all(np.isnan(vs[:tz + 1, bz])) and np.all(np.isfinite(vs[tz + 1:, bz]))
+    assert np.all(np.isnan(vs[:ty + 1, by])) and np.all(np.isfinite(vs[ty + 1:, by]))
+    assert np.all(np.isnan(np_out(out.d_logits)[tz, bz]))
+    # the lanes that share a 64-lane neighbourhood with the two rows (their
+    # waves' other lanes in every tile shape), else a spread of lanes
+    near = [b for b in list(range(0, 64)) + list(range(B - 64, B)) if b not in (bz, by)]
+    lanes = sorted(set(near + (list(range(64, B - 64, max(1, (B - 128) // 64))) if B > 128 else [])))
+    check_against_oracle(tr, p, out, lanes=lanes)
+
+
 def test_deterministic_and_workspace_reuse():
     tr = make_config(3)
     dev = to_device(tr)
