@@ -248,15 +248,16 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
       p_g = buffer_load_f32(chunk_rsrc(a.discounts, 1, 4, brow, lane_ok), os);
       p_lmu = buffer_load_f32(chunk_rsrc(a.behaviour, 1, 4, brow, lane_ok && beh_lp && !no_ratio), os);
       // Behaviour logits: one offset per lane, the columns in the instruction
-      // offset.  Columns >= A read the next lane's row (or nothing, past the
-      // array's end); the epilogue only uses columns < A.
+      // offset.  Columns >= A (the tiles' padding) get an offset beyond the
+      // descriptor, so they read nothing (they would be the next lane's row).
       const Rsrc ry = chunk_rsrc(a.behaviour, A, sizeof(BehIn), brow, lane_ok && use_y);
       const uint32_t oy = row_ok ? rel * row_y + 4u * g * static_cast<uint32_t>(sizeof(BehIn)) : kOutOfRange;
       static_for<NT>([&](auto CT) {
         constexpr int ct = decltype(CT)::value;
         static_for<4>([&](auto I) {
           constexpr int i = decltype(I)::value;
-          yreg[ct][i] = buffer_load_logit<BehIn>(ry, oy + (16 * ct + i) * sizeof(BehIn));
+          const bool col_ok = 16 * ct + 4 * g + i < A;
+          yreg[ct][i] = buffer_load_logit<BehIn>(ry, col_ok ? oy + (16 * ct + i) * sizeof(BehIn) : kOutOfRange);
         });
       });
     };

@@ -24,6 +24,8 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A >= 2 && a.A <= 
 // These are the shapes with 16-step chunks.  Batches of A = 9 or 18 that fill
 // the chip in whole generations take the long-run shapes of tiled_long_f32.hip
 // and tiled_long_bf16.hip first (64 or 128 lanes, chunks of 8 or 4 steps).
+constexpr int64_t kTwoRowMinT = 512;
+
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,
                         int64_t* num_workgroups, bool allow_multi, bool allow_long) {
   if (allow_long && (a.A == 9 || a.A == 18)) {
@@ -32,6 +34,22 @@ hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t
                               ? launch_tiled_long_f32(a, mode, st, num_workgroups, allow_multi, &err)
                               : launch_tiled_long_bf16(a, mode, st, num_workgroups, allow_multi, &err);
     if (launched) return err;
+  }
+  // A = 18 batches whose 16-lane tiles give each CU at most one workgroup
+  // (B <= 16 x CUs: one wave per SIMD) take 32-step chunks for long unrolls:
+  // two waves per SIMD and half as many chunks one after another.  Measured
+  // (loss call, fp32 logits, event-timed medians): T = 512, B = 4096 0.147 ->
+  // 0.137 ms; T = 1000, B = 4096 0.267 -> 0.248 ms and B = 2048 0.228 ->
+  // 0.200 ms.  Not taken for A = 9 (T = 512-768: 2-6% slower) nor for
+  // shorter unrolls (T = 100-200: 2-8% slower; the 30-task batch 27.7 ->
+  // 29.8 us cold), where a 32-step chunk wastes more of the last one and the
+  // latency it hides is not what bounds the call.
+  if (allow_long && a.A == 18 && a.T >= kTwoRowMinT) {
+    const int cus = compute_units();
+    if (cus > 0 && a.B <= 16 * static_cast<int64_t>(cus)) {
+      if (lt == LogitsType::F32) return launch_shape<18, 16, float, 32>(a, mode, st, num_workgroups, allow_multi);
+      return launch_shape<18, 16, uint16_t, 32>(a, mode, st, num_workgroups, allow_multi);
+    }
   }
   if (lt == LogitsType::F32) {
     if (a.A == 18) return launch_shape<18, 16, float>(a, mode, st, num_workgroups, allow_multi);

@@ -59,7 +59,8 @@ constexpr int row_shr_to_last() {
 }
 
 // L steps per chunk (16, 8 or 4): the L threads of a lane are one aligned
-// segment of a 16-lane DPP row.
+// segment of a 16-lane DPP row.  L = 32: a lane's threads are two DPP rows of
+// a wave, steps 0-15 and 16-31 of the chunk.
 template <int A_, int LANES, typename In, int L>
 struct Tile {
   static constexpr int A = A_;
@@ -75,7 +76,9 @@ struct Tile {
   static constexpr int OUT_TILE16 = L * OUT_ROW16;
   static constexpr int IN_LDS16 = L * IN_PITCH16;   // LDS footprint per tensor
   static constexpr int OUT_LDS16 = L * OUT_PITCH16;
-  static constexpr int SCAN = L == 16 ? 4 : L == 8 ? 3 : 2;  // suffix-scan stages, log2 L
+  // Suffix-scan stages within a DPP row: log2 L, and 4 for L = 32, whose
+  // lanes span two rows joined by one cross-row step.
+  static constexpr int SCAN = L >= 16 ? 4 : L == 8 ? 3 : 2;
   static constexpr int NV = (2 * IN_TILE16 + NT - 1) / NT;  // vectors per thread, both tensors
   static constexpr int NO = (OUT_TILE16 + NT - 1) / NT;     // gradient vectors per thread
   // LDS: the two logit tiles, and for the gradient kernels a separate
@@ -89,8 +92,21 @@ struct Tile {
   static_assert((SEG * 4) % 16 == 0, "gradient rows must be whole 16-byte vectors");
   static_assert(NT % kWave == 0 && NT <= 1024, "bad workgroup size");
   static_assert(OUT_ROW16 % 2 == 0, "bfloat16 gradient rows must be whole 16-byte vectors");
-  static_assert(L == 16 || L == 8 || L == 4, "steps per chunk");
+  static_assert(L == 32 || L == 16 || L == 8 || L == 4, "steps per chunk");
 };
+
+// For 32-step chunks (two lanes per wave, each on two DPP rows): x at the
+// thread of step `step` (0 or 16) of this thread's lane, i.e. at wave lane
+// step or 32 + step.  Two scalar reads per 32-bit half and a select.
+template <int kStep>
+__device__ __forceinline__ double lane_step_f64(double x, bool upper_lane) {
+  const unsigned long long u = __double_as_longlong(x);
+  const int lo = static_cast<int>(u & 0xffffffffu), hi = static_cast<int>(u >> 32);
+  const int lo0 = __builtin_amdgcn_readlane(lo, kStep), lo1 = __builtin_amdgcn_readlane(lo, 32 + kStep);
+  const int hi0 = __builtin_amdgcn_readlane(hi, kStep), hi1 = __builtin_amdgcn_readlane(hi, 32 + kStep);
+  const unsigned l = static_cast<unsigned>(upper_lane ? lo1 : lo0), h = static_cast<unsigned>(upper_lane ? hi1 : hi0);
+  return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(h) << 32) | l));
+}
 
 // Per-thread state carried along the chunk walk.
 struct Carry {
@@ -118,6 +134,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   const int tid = threadIdx.x;
   const int lane_local = tid / L;
   const int s = tid % L;
+  const int wl = tid % kWave;  // the thread's place in its wave
   const int64_t T = a.T, B = a.B;
   const int nchunks = static_cast<int>((T + L - 1) / L);
 
@@ -303,37 +320,57 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
                                           lam * clip_above(st.ratio, c_bar), lam, act_ok);
 
     const double r = r32, g = g32, V = V32;
+    // kSeg: steps of a lane within one DPP row; sr: this thread's place there.
+    constexpr int kSeg = L < 16 ? L : 16;
+    const int sr = s % kSeg;
+    const bool upper_lane = wl >= 32;  // L = 32: the wave's second lane
+    double V16 = 0.0;                  // L = 32: V(x) at step 16 of the lane
+    if constexpr (L == 32) V16 = lane_step_f64<16>(V, upper_lane);
     double V_next = dpp_f64<kRowShl1>(V);
+    if (L == 32 && s == 15) V_next = V16;
     if (s == L - 1) V_next = cy.V;
     const double delta = w.rho_v * (r + g * V_next - V);
 
     // Suffix scan over the lane's segment.  Its last step first absorbs the
     // carry from the later chunk, so that after the scan D holds v_t - V(x_t)
     // on every thread: (G, D) composes the maps of steps s..L-1 applied to
-    // that carry.
+    // that carry.  With 32 steps the scan runs in each DPP row, and the lower
+    // row then composes its maps with the upper row's first step.
     double G = g * w.c_v, D = delta;
     if (s == L - 1) D = fma(G, cy.A, D);
     static_for<S::SCAN>([&](auto I) {
       constexpr int off = 1 << decltype(I)::value;
       const double Gn = dpp_f64<0x100 + off>(G);
       const double Dn = dpp_f64<0x100 + off>(D);
-      if (s + off < L) {
+      if (sr + off < kSeg) {
         D = fma(G, Dn, D);
         G = G * Gn;
       }
     });
+    double D16 = 0.0;  // L = 32: v - V(x) at step 16 of the lane
+    if constexpr (L == 32) {
+      D16 = lane_step_f64<16>(D, upper_lane);
+      if (s < 16) D = fma(G, D16, D);
+    }
     const double A_t = D;  // v_t - V(x_t)
     const double v_t = V + A_t;
     double v_next = dpp_f64<kRowShl1>(v_t);
+    if (L == 32 && s == 15) v_next = V16 + D16;
     if (s == L - 1) v_next = cy.v;
     const double q_next = q_estimate == kQBaseline ? V_next : v_next;
     const double adv = w.rho_pg * (r + g * q_next - V);
 
     // The segment's first step becomes the carry of the earlier chunk, held by
     // the segment's last thread, the only one that reads it.
-    cy.A = dpp_f64<row_shr_to_last<L>()>(A_t);
-    cy.v = dpp_f64<row_shr_to_last<L>()>(v_t);
-    cy.V = dpp_f64<row_shr_to_last<L>()>(V);
+    if constexpr (L == 32) {
+      cy.A = lane_step_f64<0>(A_t, upper_lane);
+      cy.v = lane_step_f64<0>(v_t, upper_lane);
+      cy.V = lane_step_f64<0>(V, upper_lane);
+    } else {
+      cy.A = dpp_f64<row_shr_to_last<L>()>(A_t);
+      cy.v = dpp_f64<row_shr_to_last<L>()>(v_t);
+      cy.V = dpp_f64<row_shr_to_last<L>()>(V);
+    }
 
     if (step_ok) {
       if constexpr (kVec) {

@@ -605,6 +605,28 @@ def test_long_run_tile_shapes_short_unrolls(lanes_per_cu, T, monkeypatch):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("T,B,A,bf16", [(512, 4096, 18, False), (513, 4096, 18, False), (544, 4091, 18, True),
+                                         (1000, 2048, 18, False), (543, 1000, 18, True)])
+def test_two_row_chunks(T, B, A, bf16):
+    """Batches of at most 16 lanes per CU with A = 18 and T >= 512 take
+    32-step chunks (two lanes per wave, each on two DPP rows joined by one
+    cross-row step of the scan): whole chunks, one step more than whole
+    chunks, a lane tile cut short (element path), bf16 logits, every output
+    against the oracle, for the loss call and the targets-only call."""
+    tr = make_random(T, B, A, 5100 + T + B, noise_std=1.0, end_prob=0.02, bf16=bf16)
+    dev = to_device(tr)
+    p = PARAM_SETS[4][1] if T == 513 else PARAM_SETS[4][0]
+    log_case(f"32-step chunks T={T} B={B} A={A} bf16={bf16}")
+    check_against_oracle(tr, p, run_loss_grad(dev, p))
+    vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
+    torch.cuda.synchronize()
+    ot = oracle.vtrace(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam)
+    assert_close("targets.vs", np_out(vs), ot.vs)
+    assert_close("targets.pg_advantages", np_out(pg), ot.pg_advantages)
+    del dev
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("kernel", ["tiled", "wide"])
 @pytest.mark.parametrize("cfg,bf16", [(0, False), (1, False), (2, False), (3, False), (3, True),
                                       (2, True)])
