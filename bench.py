@@ -548,6 +548,23 @@ def main():
             "traffic": traffic,
         },
     }
+    if is_counted_workload and len(PARAM_SETS[args.config]) > 1:
+        # The stress batch's other parameter sets on the same inputs (fewer
+        # calls each, after the timed region): every set is held to the same
+        # tolerance and takes the same kernel.
+        others = []
+        for q in PARAM_SETS[args.config][1:]:
+            def step_q(q=q):
+                vt.vtrace_loss_grad(**dev, rho_bar=q.rho_bar, c_bar=q.c_bar, lam=q.lam,
+                                    baseline_cost=q.baseline_cost, entropy_cost=q.entropy_cost,
+                                    workspace=ws, out=out, grad_dtype=grad_dtype)
+            q_ms, _ = timed_calls(step_q, max(10, K // 5), 3, stream, None)
+            q_avg = float(q_ms.mean())
+            others.append({"rho_bar": q.rho_bar if math.isfinite(q.rho_bar) else "inf",
+                           "c_bar": q.c_bar if math.isfinite(q.c_bar) else "inf", "lambda": q.lam,
+                           "calls": int(q_ms.size), "kernel_ms_avg": q_avg,
+                           "frac": alg_bytes / (q_avg * 1e-3) / 1e9 / PEAK_HBM_GBS})
+        result["other_param_sets"] = others
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(tr, p, args.cpu_seconds)
     print(json.dumps(result), flush=True)
