@@ -75,8 +75,9 @@ __device__ __forceinline__ float read_row_max(const In* r, float (&v)[A_]) {
 
 // Whether every row of the wave is finite (its maximum m and its minimum
 // both finite): then no exponent-sum term needs the clamp against -inf and
-// NaN logits, and the whole wave takes the unclamped terms (36 VALU
-// instructions fewer per step for 9 to find the minimum).
+// NaN logits, and the whole wave takes the unclamped terms (A + 1 VALU
+// instructions fewer per row for the A - 1 that find its minimum, fewer for
+// three-operand minima).  Called by every thread of the wave.
 template <int A_>
 __device__ __forceinline__ bool wave_rows_finite(const float (&v)[A_], float m) {
   float mn = v[0];

@@ -311,8 +311,8 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     // use neither.
     static_assert(!kGrad || kPrecise, "loss kernels form their exponent sums in float64");
     constexpr bool kRowRegs = kGrad && kPlain;
-    float* const lo = reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_;
     float e_reg[A_], z_reg[A_];
+    float* const lo = kGrad ? reinterpret_cast<float*>(lds_g) + s * S::OUT_PITCH + lane_local * A_ : e_reg;
     float* const e_out = kGrad && !kRowRegs ? lo : e_reg;
     RowStats st = row_stats<A_, kPrecise>(zr, yr, act_c, act_ok, beh_lp, no_ratio, lmu, e_out,
                                           kRowRegs ? z_reg : nullptr);

@@ -538,17 +538,18 @@ def test_multi_tile_walk_unroll_lengths(T, monkeypatch):
 @pytest.mark.parametrize("lanes_per_cu", [64, 128, 192, 256])
 def test_long_run_tile_shapes(A, bf16, lanes_per_cu, monkeypatch):
     """Batches of 64, 128, 192 and 256 lanes per CU take the long-run tile
-    shapes where the float32 ratio mode applies (64 x 8, 128 x 4 or 64 x 4
-    lanes x steps per chunk, and 32 x 8 or 64 x 4 for bf16 logits with A = 9;
-    64 x 4 through the multi-tile walk where the batch is a whole number of its
-    generations; 192 lanes per CU as three generations of 64 x 8 for fp32
-    logits).  T = 37 leaves every chunk length a ragged last chunk.  Every
-    output against the oracle, with weights clipped at 1, with (1, 0.5, 0.95),
-    and unclipped (which takes the float64 ratio mode and the 16-step tiles);
-    the targets-only call against the oracle; the 16-step tiles
-    (VTRACE_KERNEL=tiled_short) within the tolerance; and one workgroup per tile
-    (tiled_single, the same shape without the multi-tile walk) bit-identical
-    per step and per lane."""
+    shapes: the loss call with A = 18 the 32 x 8 loss tiles (one to four
+    whole generations of them; A = 9 keeps the 16-step tiles), the targets-only
+    call in the float32 ratio mode 64 x 8, 128 x 4 or 64 x 4 lanes x steps per
+    chunk (32 x 8 or 64 x 4 for bf16 logits with A = 9; 64 x 4 through the
+    multi-tile walk where the batch is a whole number of its generations; 192
+    lanes per CU as three generations of 64 x 8 for fp32 logits), and with
+    unclipped weights (float64 sums) the 16-step tiles.  T = 37 leaves every
+    chunk length a ragged last chunk.  Every output against the oracle, with
+    weights clipped at 1, with (1, 0.5, 0.95) and unclipped; the targets-only
+    call against the oracle; the 16-step tiles (VTRACE_KERNEL=tiled_short)
+    within the tolerance; and one workgroup per tile (tiled_single, the same
+    shape without the multi-tile walk) bit-identical per step and per lane."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     T, B = 37, lanes_per_cu * cus
     tr = make_random(T, B, A, 3000 + A + lanes_per_cu, noise_std=1.0, end_prob=0.03, bf16=bf16)
