@@ -486,6 +486,7 @@ def main():
         flush_buf = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
         flush = lambda: flush_buf.fill_(1)  # noqa: E731
     kernel_ms, ms_per_step = timed_calls(step, K, args.warmup, stream, flush)
+    main_losses = out.losses.clone()  # on the stream: the sets below reuse `out`
     is_counted_workload = (args.config == 4 and args.params == 0 and not args.bf16
                            and args.kernel == "auto" and args.correction == "vtrace"
                            and not args.log_probs and not args.grad_bf16
@@ -513,7 +514,7 @@ def main():
                                             args.correction in ("vtrace", "one_step_is"))
     avg_kernel_ms = float(kernel_ms.mean())
     achieved = alg_bytes / (avg_kernel_ms * 1e-3) / 1e9
-    losses = out.losses.cpu().tolist()
+    losses = main_losses.cpu().tolist()
     print(f"[bench] kernel avg {avg_kernel_ms:.4f} ms (min {kernel_ms.min():.4f}, median "
           f"{np.median(kernel_ms):.4f}); wall {ms_per_step:.4f} ms/step; {achieved:.1f} GB/s "
           f"algorithmic; losses {losses}", file=sys.stderr, flush=True)
