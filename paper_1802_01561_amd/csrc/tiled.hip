@@ -23,7 +23,7 @@ bool tiled_supported(const StepArgs& a, LogitsType) { return a.A >= 2 && a.A <= 
 //
 // These are the shapes with 16-step chunks.  Batches of A = 9 or 18 that fill
 // the chip in whole generations take the long-run shapes of tiled_long_f32.hip
-// and tiled_long_bf16.hip first (64 or 128 lanes, chunks of 8 or 4 steps).
+// and tiled_long_bf16.hip first (32 to 128 lanes, chunks of 8 or 4 steps).
 constexpr int64_t kTwoRowMinT = 512;
 
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t st,

@@ -1,17 +1,24 @@
-// Long-run tile shapes for bfloat16 logits, A = 9 and A = 18 (the kernel is in
-// tiled_impl.hpp).  Measured at T = 1000 against the 16-step tiles: A = 18,
-// 16384 lanes 0.572 -> 0.507 ms (64 lanes x 8 steps), 32768 lanes 1.12 ->
-// 0.98 ms (128 x 4); A = 9, 16384 lanes 0.435 -> 0.348 ms (32 x 8), 32768
-// lanes 0.788 -> 0.632 ms (64 x 4).  For A = 9 the 512-thread shapes measured
-// slower than these (one workgroup per CU).
+// Long-run tile shapes for bfloat16 logits, A = 9 and A = 18 (the kernel is
+// in tiled_impl.hpp).  Event-timed medians at T = 1000 against the 16-step
+// tiles (VTRACE_KERNEL=tiled_short):
+//   targets-only call: A = 18, 16384 lanes 0.405 -> 0.340 ms; A = 9, 16384
+//   lanes 0.347 -> 0.275 ms, 32768 lanes 0.645 -> 0.514 ms.  For A = 9 the
+//   512-thread shapes measured slower than these (one workgroup per CU);
+//   loss call (float64 row sums): A = 18, 16384 lanes 0.706 -> 0.668 ms
+//   (32 x 8; 64 x 8 0.683); A = 9, 16384 lanes 0.441 -> 0.396 ms (32 x 8),
+//   32768 lanes 0.820 -> 0.746 ms (64 x 4; 32 x 8 0.747, 64 x 8 0.771).
 #include "tiled_impl.hpp"
 
 namespace vtrace {
 
 bool launch_tiled_long_bf16(const StepArgs& a, Mode mode, hipStream_t st, int64_t* num_workgroups,
                             bool allow_multi, hipError_t* err) {
-  // Loss calls with A = 18: 32 lanes x 8 steps (2304-byte runs per time row).
-  if (mode == Mode::LossGrad) return a.A == 18 && launch_long_loss<18, uint16_t, Shape<32, 8>>(a, st, num_workgroups, err);
+  // Loss calls: A = 18 32 lanes x 8 steps (1152-byte runs per time row); A = 9
+  // 64 x 4 where its tiles make whole generations, else 32 x 8.
+  if (mode == Mode::LossGrad) {
+    if (a.A == 18) return launch_long_loss<18, uint16_t, Shape<32, 8>>(a, st, num_workgroups, err);
+    return a.A == 9 && launch_long_loss<9, uint16_t, Shape<64, 4>, Shape<32, 8>>(a, st, num_workgroups, err);
+  }
   if (a.A == 18)
     return launch_long<18, uint16_t, Shape<128, 4>, Shape<64, 8>, Shape<64, 4>>(a, mode, st, num_workgroups,
                                                                                allow_multi, err);

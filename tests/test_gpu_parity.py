@@ -539,7 +539,8 @@ def test_multi_tile_walk_unroll_lengths(T, monkeypatch):
 def test_long_run_tile_shapes(A, bf16, lanes_per_cu, monkeypatch):
     """Batches of 64, 128, 192 and 256 lanes per CU take the long-run tile
     shapes: the loss call with A = 18 the 32 x 8 loss tiles (one to four
-    whole generations of them; A = 9 keeps the 16-step tiles), the targets-only
+    whole generations of them), with A = 9 64 x 4 (128 and 256 lanes per CU)
+    or 32 x 8 (64 and 192 lanes per CU), the targets-only
     call in the float32 ratio mode 64 x 8, 128 x 4 or 64 x 4 lanes x steps per
     chunk (32 x 8 or 64 x 4 for bf16 logits with A = 9; 64 x 4 through the
     multi-tile walk where the batch is a whole number of its generations; 192
