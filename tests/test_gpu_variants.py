@@ -223,8 +223,8 @@ def _sweep_cases():
     cases.append(dict(T=20, B=24576, A=18, bf16=False, p=Params(1.0, 0.5, 0.95), correction="one_step_is",
                       q_estimate="baseline", log_probs=False, reward_transform=None, grad_bf16=False,
                       lanes=[3, 777, 24560, 24575]))
-    # 64 lanes per CU on a 256-CU part: the long-run tile shapes (64 x 8; 32 x 8
-    # for bf16 logits with A = 9), with ragged T, on a lane subset
+    # 64 lanes per CU on a 256-CU part: the long-run tile shapes (loss calls:
+    # 32 x 8 for A = 9 and 18), with ragged T, on a lane subset
     for A, bf16, lp, gb, corr, qe, rt in [(18, False, True, True, "one_step_is", "vtrace", "asymmetric"),
                                           (9, False, False, True, "epsilon", "baseline", "clip"),
                                           (18, True, True, False, "none", "vtrace", None),
@@ -232,6 +232,11 @@ def _sweep_cases():
         cases.append(dict(T=37, B=16384, A=A, bf16=bf16, p=Params(1.0, 0.5, 0.95), correction=corr,
                           q_estimate=qe, log_probs=lp, reward_transform=rt, grad_bf16=gb,
                           lanes=[0, 1, 31, 32, 63, 64, 8191, 16320, 16383]))
+    # 128 lanes per CU: loss calls with A = 9 take 64 x 4 tiles
+    for bf16, lp, gb, corr, qe in [(False, True, False, "epsilon", "vtrace"), (True, False, True, "one_step_is", "baseline")]:
+        cases.append(dict(T=21, B=32768, A=9, bf16=bf16, p=Params(2.0, 1.0, 0.9), correction=corr,
+                          q_estimate=qe, log_probs=lp, reward_transform="clip", grad_bf16=gb,
+                          lanes=[0, 1, 63, 64, 127, 16383, 16384, 32704, 32767]))
     return cases
 
 
@@ -242,8 +247,9 @@ def test_random_sweep(i):
     bfloat16 gradients and clipping levels, each against the oracle; then
     batches of 24576 lanes, whole multiples of the workgroups the chip holds at
     once, which take the tiled kernel's multi-tile walk (bf16 logits with
-    A = 9: the 32 x 8 long-run tiles, which fill the chip once there), and of
-    16384 lanes, which take the long-run tile shapes."""
+    A = 9: the 32 x 8 long-run tiles, which fill the chip once there), of
+    16384 lanes, which take the long-run tile shapes, and of 32768 lanes with
+    A = 9, whose loss calls take 64 x 4 tiles."""
     c = _sweep_cases()[i]
     tr = make_random(c["T"], c["B"], c["A"], 900 + i, noise_std=1.0, end_prob=0.03, bf16=c["bf16"])
     tr.rewards = (tr.rewards * 2.5).astype(np.float32)  # exercise the clipping
