@@ -68,8 +68,9 @@ constexpr int64_t kTiledMaxActions = 20;
 // tile shapes).
 hipError_t launch_tiled(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s,
                         int64_t* num_workgroups, bool allow_multi, bool allow_long);
-// Long-run tile shapes for A = 9 and A = 18 in the float32 ratio mode: true
-// (with the launch status in *err) when one applies and was launched.
+// Long-run tile shapes for A = 9 and A = 18 (targets-only calls in the float32
+// ratio mode; loss calls by a rule of their own): true (with the launch
+// status in *err) when one applies and was launched.
 bool launch_tiled_long_f32(const StepArgs& a, Mode mode, hipStream_t s, int64_t* num_workgroups,
                            bool allow_multi, hipError_t* err);
 bool launch_tiled_long_bf16(const StepArgs& a, Mode mode, hipStream_t s, int64_t* num_workgroups,
