@@ -64,12 +64,18 @@ Kernel forced_kernel() {
 }
 
 // Where both apply, the time-parallel kernel wins while the tiled kernel's
-// serial walk over T / 16 chunks takes longer than the time-parallel kernel's
-// uncoalesced row reads: measured on MI355X (A = 9 and 18, T from 20 to 256,
-// B from 8 to 2048), that is for more than two chunks and B <= 128, or B <= 512
-// with T <= 100.  (The DMLab-shaped batch, T = 100 and B = 32, takes it.)
-bool prefer_wide(const StepArgs& a) {
-  return a.T > 32 && a.T <= 256 && (a.B <= 128 || (a.B <= 512 && a.T <= 100));
+// serial walk over T / 16 chunks costs more than the time-parallel kernel's
+// uncoalesced row reads.  Measured on MI355X (cold, A = 9 and 18, T from 16
+// to 256, B from 8 to 2048, fp32 logits): batches of fewer than 16 lanes (less
+// than one lane tile) at every T; loss calls of more than one chunk and
+// targets-only calls of more than two, with B <= 512, or with B <= 1024 and
+// T <= 128 (for loss calls only with A = 18).  The DMLab- and Atari-shaped
+// batches (B = 32, T = 100 and 20) take it.
+bool prefer_wide(const StepArgs& a, Mode mode) {
+  if (a.B < 16) return true;
+  const bool loss = mode == Mode::LossGrad;
+  if (a.T <= (loss ? 16 : 32)) return false;
+  return a.B <= 512 || (a.B <= 1024 && a.T <= 128 && (!loss || a.A >= 18));
 }
 
 size_t workspace_bytes_for(int64_t B) {
@@ -183,7 +189,7 @@ vtrace_status launch(const StepArgs& a, LogitsType lt, Mode mode, hipStream_t s)
   const bool tiled = vtrace::tiled_supported(a, lt);
   if (k == Kernel::LaneSerial)
     e = vtrace::launch_lane_serial(a, lt, mode, s, &nwg);
-  else if (wide && (k == Kernel::Wide || (k == Kernel::Auto && prefer_wide(a))))
+  else if (wide && (k == Kernel::Wide || (k == Kernel::Auto && prefer_wide(a, mode))))
     e = vtrace::launch_wide(a, lt, mode, s, &nwg);
   else if (tiled)
     e = vtrace::launch_tiled(a, lt, mode, s, &nwg, k != Kernel::TiledSingle && k != Kernel::TiledShortSingle,

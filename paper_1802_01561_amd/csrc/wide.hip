@@ -16,7 +16,10 @@
 // Steps at or beyond T carry the identity-breaking map (0, 0), which makes
 // v_{T-1} use V(x_T) exactly as Eq. (1) does.  Each thread reads its own logit
 // rows straight from global memory: at these sizes latency, not bandwidth,
-// sets the time.
+// sets the time.  The loss kernel's outputs go through LDS instead: the first
+// wave reduces the losses and takes the cross-workgroup ticket while the
+// other three store every output in runs of whole time rows, so that the
+// wait before the ticket and the gradient stores overlap instead of adding.
 #include "device_common.hpp"
 #include "row_stats.hpp"
 #include "wave_ops.hpp"
@@ -24,16 +27,71 @@
 namespace vtrace {
 namespace {
 
-constexpr int kWideThreads = 256;
+constexpr int kWideLog2 = 8;
+constexpr int kWideThreads = 1 << kWideLog2;
 constexpr int kRow = 16;
 constexpr int kRows = kWideThreads / kRow;
+
+// The loss reduction of the loss kernel, run by its first wave alone while the
+// other waves store the outputs: each lane passes its share of the
+// workgroup's three sums (added in a fixed order), and the cross-workgroup
+// step is finish_losses' ticket.  This wave stores nothing but lane losses
+// before its partial, so the wait for the partial's stores before the ticket
+// does not also wait for the gradient stores.
+__device__ void finish_losses_first_wave(const StepArgs& a, double pg, double base, double ent) {
+  pg = wave_sum(pg);
+  base = wave_sum(base);
+  ent = wave_sum(ent);
+  const bool lead = threadIdx.x == 0;
+  if (gridDim.x == 1) {
+    if (lead) {
+      a.losses[0] = static_cast<float>(pg + base + ent);
+      a.losses[1] = static_cast<float>(pg);
+      a.losses[2] = static_cast<float>(base);
+      a.losses[3] = static_cast<float>(ent);
+    }
+    return;
+  }
+  int last = 0;
+  if (lead) {
+    double* p = a.partials + 3 * static_cast<size_t>(blockIdx.x);
+    __hip_atomic_store(p + 0, pg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 1, base, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p + 2, ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);  // the partial stores have completed
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    const unsigned prev = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last = prev == gridDim.x - 1;
+  }
+  if (__shfl(last, 0, kWave) == 0) return;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0;
+  for (unsigned i = threadIdx.x; i < gridDim.x; i += kWave) {
+    const double* p = a.partials + 3 * static_cast<size_t>(i);
+    s0 += __hip_atomic_load(p + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s1 += __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s2 += __hip_atomic_load(p + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  s0 = wave_sum(s0);
+  s1 = wave_sum(s1);
+  s2 = wave_sum(s2);
+  if (lead) {
+    a.losses[0] = static_cast<float>(s0 + s1 + s2);
+    a.losses[1] = static_cast<float>(s0);
+    a.losses[2] = static_cast<float>(s1);
+    a.losses[3] = static_cast<float>(s2);
+    __hip_atomic_store(a.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
 
 template <int A_, typename In, bool kGrad, bool kPrecise>
 __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_log2) {
   __shared__ double s_x[kWideThreads];    // V(x_t), then v_t, by thread
   __shared__ double s_g[kRows], s_d[kRows], s_c[kRows];
   __shared__ double s_loss[3 * kRows];
-  __shared__ double red_scratch[3 * (kWideThreads / kWave)];
+  // Loss kernel outputs by time row (position t * lanes + lane): d_logits
+  // rows, then d_values, v_s and the advantages.
+  __shared__ float s_out[kGrad ? kWideThreads * (A_ + 3) : 1];
 
   const int tp = 1 << tp_log2;
   const int tid = threadIdx.x;
@@ -110,12 +168,12 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
   const double q_next = a.q_estimate == kQBaseline ? V_next : v_next;
   const double adv = w.rho_pg * (r + gm * q_next - V);
 
-  if (step_ok) {
-    if (a.vs) a.vs[idx] = static_cast<float>(v_t);
-    if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
-  }
-
-  if constexpr (kGrad) {
+  if constexpr (!kGrad) {
+    if (step_ok) {
+      if (a.vs) a.vs[idx] = static_cast<float>(v_t);
+      if (a.pg_adv) a.pg_adv[idx] = static_cast<float>(adv);
+    }
+  } else {
     // d_logits_j = adv (pi_j - 1[j=a]) + ce pi_j (log pi_j + H): e_j (alpha +
     // beta z_j) off the taken action, as in the tiled kernel.
     const float ce = a.entropy_cost;
@@ -128,26 +186,32 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
     const float alpha = st.inv_s * adv32 - beta * K;
     const float za = logit_to_float(zr[act_c]);
     const float out_a = -adv32 * st.one_minus_pa + ce * pa * (za - K);
+    // The outputs go to LDS in time-row order, where the workgroup's lanes of
+    // one step are one contiguous run, as in memory.
+    const int lanes_log2 = kWideLog2 - tp_log2;
+    const int pos = (t << lanes_log2) + lane_local;
+    float* const s_dl = s_out;                           // [tp * lanes][A]
+    float* const s_dv = s_out + kWideThreads * A_;      // [tp * lanes]
+    float* const s_vs = s_dv + kWideThreads;
+    float* const s_pa = s_vs + kWideThreads;
     double l_pg = 0.0, l_base = 0.0, l_ent = 0.0;
     if (step_ok) {
-      a.d_values[idx] = static_cast<float>(a.baseline_cost * (V - v_t));
+      s_dv[pos] = static_cast<float>(a.baseline_cost * (V - v_t));
+      s_vs[pos] = static_cast<float>(v_t);
+      s_pa[pos] = static_cast<float>(adv);
       const double log_pa = !act_ok ? NAN : eps_mode ? log_prob_plus_eps<kPrecise>(st, a.epsilon) : st.log_pa;
       l_pg = -adv * log_pa;
       l_base = 0.5 * A_t * A_t;
       l_ent = -static_cast<double>(st.H);
-      const bool bf16 = a.grad_bf16 != 0;
 #pragma unroll
       for (int j = 0; j < A_; ++j) {
         float x = e[j] * fmaf(beta, logit_to_float(zr[j]), alpha);
         if (j == act_c) x = act_ok ? out_a : NAN;
-        if (bf16)
-          static_cast<uint16_t*>(a.d_logits)[idx * A_ + j] = to_bf16(x);
-        else
-          static_cast<float*>(a.d_logits)[idx * A_ + j] = x;
+        s_dl[pos * A_ + j] = x;
       }
     }
     // Loss sums: per row (fixed butterfly), per lane (rows in order), then
-    // over the batch.
+    // over the workgroup's lanes and the batch.
 #pragma unroll
     for (int off = kRow / 2; off > 0; off >>= 1) {
       l_pg += __shfl_xor(l_pg, off, kRow);
@@ -160,23 +224,56 @@ __global__ __launch_bounds__(kWideThreads) void wide_kernel(StepArgs a, int tp_l
       s_loss[3 * row + 2] = l_ent;
     }
     __syncthreads();
-    double pg = 0.0, base = 0.0, ent = 0.0;
-    if (t == 0) {
-      for (int rr = 0; rr < rows_per_lane; ++rr) {
-        pg += s_loss[3 * (row + rr) + 0];
-        base += s_loss[3 * (row + rr) + 1];
-        ent += s_loss[3 * (row + rr) + 2];
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * lanes;
+    if (tid < kWave) {
+      // First wave: the loss sums, lane tid of the workgroup in thread tid.
+      double pg = 0.0, base = 0.0, ent = 0.0;
+      if (tid < lanes) {
+        for (int rr = 0; rr < rows_per_lane; ++rr) {
+          const int q = tid * rows_per_lane + rr;
+          pg += s_loss[3 * q + 0];
+          base += s_loss[3 * q + 1];
+          ent += s_loss[3 * q + 2];
+        }
+        base *= a.baseline_cost;
+        ent *= a.entropy_cost;
+        const int64_t bl = b0 + tid;
+        if (bl < B && a.lane_losses) {
+          a.lane_losses[3 * bl + 0] = static_cast<float>(pg);
+          a.lane_losses[3 * bl + 1] = static_cast<float>(base);
+          a.lane_losses[3 * bl + 2] = static_cast<float>(ent);
+        }
+        if (bl >= B) pg = base = ent = 0.0;
       }
-      base *= a.baseline_cost;
-      ent *= a.entropy_cost;
-      if (lane_ok && a.lane_losses) {
-        a.lane_losses[3 * b + 0] = static_cast<float>(pg);
-        a.lane_losses[3 * b + 1] = static_cast<float>(base);
-        a.lane_losses[3 * b + 2] = static_cast<float>(ent);
+      finish_losses_first_wave(a, pg, base, ent);
+    } else {
+      // The other waves: coalesced stores of the outputs, time row by time row.
+      constexpr int kCopy = kWideThreads - kWave;
+      const int k = tid - kWave;
+      const bool bf16 = a.grad_bf16 != 0;
+      for (int f = k; f < kWideThreads * A_; f += kCopy) {
+        const int q = f / A_;
+        const int tt = q >> lanes_log2;
+        const int ll = q & (lanes - 1);
+        if (tt < T && b0 + ll < B) {
+          const int64_t g = (static_cast<int64_t>(tt) * B + b0 + ll) * A_ + (f - q * A_);
+          if (bf16)
+            static_cast<uint16_t*>(a.d_logits)[g] = to_bf16(s_dl[f]);
+          else
+            static_cast<float*>(a.d_logits)[g] = s_dl[f];
+        }
       }
-      if (!lane_ok) pg = base = ent = 0.0;
+      for (int q = k; q < kWideThreads; q += kCopy) {
+        const int tt = q >> lanes_log2;
+        const int ll = q & (lanes - 1);
+        if (tt < T && b0 + ll < B) {
+          const int64_t g = static_cast<int64_t>(tt) * B + b0 + ll;
+          a.d_values[g] = s_dv[q];
+          if (a.vs) a.vs[g] = s_vs[q];
+          if (a.pg_adv) a.pg_adv[g] = s_pa[q];
+        }
+      }
     }
-    finish_losses<kWideThreads>(a, pg, base, ent, red_scratch);
   }
 }
 

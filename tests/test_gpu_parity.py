@@ -634,7 +634,7 @@ def test_two_row_chunks(T, B, A, bf16):
                                       (2, True)])
 def test_config_each_kernel(cfg, bf16, kernel, monkeypatch):
     """Configs 0-3 through each of the two fast kernels (the automatic choice
-    takes the time-parallel one for these shapes)."""
+    takes the time-parallel one for configs 0-2, the tiled one for config 3)."""
     monkeypatch.setenv("VTRACE_KERNEL", kernel)
     tr = make_config(cfg, bf16=bf16)
     dev = to_device(tr)
