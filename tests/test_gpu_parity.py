@@ -643,6 +643,56 @@ def test_config_each_kernel(cfg, bf16, kernel, monkeypatch):
         check_against_oracle(tr, p, run_loss_grad(dev, p))
 
 
+# (T, B, A, bf16 logits, kernel the automatic choice takes): the paper's
+# learner batches and shapes on both sides of the measured crossover, each
+# with a different workgroup count under the two kernels.
+CHOICE_CASES = [(100, 32, 9, False, "wide"), (20, 32, 18, False, "wide"), (48, 8, 18, False, "wide"),
+                (64, 1024, 18, False, "wide"), (16, 32, 18, True, "tiled"), (64, 1024, 9, False, "tiled"),
+                (100, 4096, 9, False, "tiled"), (300, 32, 9, False, "tiled")]
+_PARTIAL_SENTINEL = 0x7FF4DEADBEEF0001  # a NaN no partial sum can take
+
+
+def _call_counting_workgroups(dev, p, T, B, A):
+    """One loss call on a fresh workspace whose partials are preset to a
+    sentinel; returns the outputs and the number of workgroups that wrote a
+    loss partial.  (The workspace is a 256-byte header followed by three
+    float64 partials per workgroup, the layout VTRACE_STATIC_WORKSPACE_BYTES
+    states; a single-workgroup grid writes none.)"""
+    ws = vt.Workspace(T, B, A, device="cuda")
+    parts = ws.tensor[256:].view(torch.int64)
+    parts.fill_(_PARTIAL_SENTINEL)
+    out = run_loss_grad(dev, p, workspace=ws)
+    written = int((parts != _PARTIAL_SENTINEL).sum().item())
+    assert written % 3 == 0
+    return out, written // 3
+
+
+@pytest.mark.parametrize("T,B,A,bf16,kernel", CHOICE_CASES)
+def test_automatic_kernel_choice(T, B, A, bf16, kernel, monkeypatch):
+    """The automatic choice between the time-parallel and the tiled kernel.
+    The two give the same float32 outputs (their float64 sums differ only far
+    below float32 resolution), so they are told apart by their grids: the
+    automatic call runs as many workgroups as the forced kernel and a
+    different number from the other one, and matches the forced kernel bit
+    for bit."""
+    tr = make_random(T, B, A, 7000 + T + B + A, noise_std=1.0, end_prob=0.02, bf16=bf16)
+    dev = to_device(tr)
+    p = PARAM_SETS[4][0]
+    log_case(f"kernel choice T={T} B={B} A={A} bf16={bf16} -> {kernel}")
+    monkeypatch.delenv("VTRACE_KERNEL", raising=False)
+    auto, n_auto = _call_counting_workgroups(dev, p, T, B, A)
+    monkeypatch.setenv("VTRACE_KERNEL", kernel)
+    forced, n_forced = _call_counting_workgroups(dev, p, T, B, A)
+    if T <= 256:
+        monkeypatch.setenv("VTRACE_KERNEL", "tiled" if kernel == "wide" else "wide")
+        _, n_other = _call_counting_workgroups(dev, p, T, B, A)
+        assert n_other != n_forced, "the two kernels run as many workgroups: the case cannot tell them apart"
+    monkeypatch.delenv("VTRACE_KERNEL")
+    assert n_auto == n_forced, f"the automatic call ran {n_auto} workgroups, the {kernel} kernel {n_forced}"
+    for name in ("vs", "pg_advantages", "d_values", "d_logits", "lane_losses", "losses"):
+        assert np.array_equal(_bits(getattr(auto, name)), _bits(getattr(forced, name))), name
+
+
 WIDE_SHAPES = [(1, 1, 9), (1, 300, 18), (16, 16, 18), (17, 7, 9), (31, 5, 18), (64, 9, 9),
                (100, 33, 18), (128, 4, 9), (129, 3, 9), (200, 2, 18), (256, 3, 9), (255, 1, 18)]
 
