@@ -114,13 +114,19 @@ struct Carry {
   double pg, base, ent;
 };
 
+// Which variant switches a kernel takes at run time: all of them (kGeneralCall),
+// none (kPlainCall: plain V-trace, is_plain_vtrace), or only the reward
+// transform (kPlainRewards: is_plain_vtrace_any_rewards).
+constexpr int kGeneralCall = 0;
+constexpr int kPlainCall = 1;
+constexpr int kPlainRewards = 2;
 
 // Walks one tile (kMulti false: `tile`, with the carry cy set up by the
 // caller), or (kMulti true, vector tiles only) the tiles first_tile + i *
 // tile_stride, i < ntiles, one after another as one loop over their chunks, so
 // that the prefetch runs across tile boundaries; each lane's loss totals are
 // then added to acc[3 * lane], a slot only the lane's step-0 thread touches.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kVec, bool kMulti, bool kPlain>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kVec, bool kMulti, int kPlain>
 __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t first_tile,
                                            int64_t tile_stride, int64_t ntiles, Carry& cy,
                                            double* acc) {
@@ -140,12 +146,13 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
 
   // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
-  // kPlain: the call is plain V-trace (logits of both policies, rewards as
-  // given, q_s from v_{s+1}, float32 gradients), so every variant switch below
-  // is a compile-time constant.
+  // kPlain: the call is plain V-trace (logits of both policies, q_s from
+  // v_{s+1}, float32 gradients), so every variant switch below is a
+  // compile-time constant; kPlainCall also has rewards as given, while
+  // kPlainRewards keeps the reward transform a run-time switch.
   const int correction = kPlain ? kCorrVtrace : a.correction;
   const int q_estimate = kPlain ? 0 : a.q_estimate;
-  const int reward_transform = kPlain ? 0 : a.reward_transform;
+  const int reward_transform = kPlain == kPlainCall ? 0 : a.reward_transform;
   const bool beh_lp = !kPlain && a.behaviour_log_probs != 0;
   // No-correction and epsilon-correction never look at the behaviour policy.
   const bool no_ratio = correction == kCorrNone || correction == kCorrEpsilon;
@@ -516,7 +523,7 @@ __device__ __forceinline__ int64_t first_tile_of_workgroup() {
 // workgroups whenever a slot frees, and leave the chip partly idle at the end.
 // The fp64 ratio mode with A > 18 is asked for two waves per SIMD explicitly:
 // left to itself the compiler gives A = 19 two registers more than fit.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kMulti, bool kPlain = false>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kMulti, int kPlain = kGeneralCall>
 __global__ __launch_bounds__(LANES* L, (kPrecise && A_ >= 18) ? 2 : 1) void tiled_kernel(
     StepArgs a, int64_t num_vec_tiles, int64_t tiles_per_wg) {
   using S = Tile<A_, LANES, In, L>;
@@ -645,7 +652,7 @@ int compute_units() {
 // the longer walk, and with one resident workgroup per CU (the 512-thread
 // kernel of bfloat16 logits with A = 18) the multi-tile walk measured 4-10%
 // slower.
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, bool kPlain = false>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kPrecise, int kPlain = kGeneralCall>
 int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                       bool allow_multi) {
   if constexpr (!kPrecise) {
@@ -667,11 +674,16 @@ int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t 
 // Loss kernels always take the float64 exponent sums; a targets-only call
 // takes them when its weights can amplify ratio errors.  kFastOnly: only the
 // float32 mode is instantiated (the caller has checked precise_row_sums).
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly, bool kRewardsPlain = false>
 int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                     bool allow_multi) {
   if constexpr (kGrad) {
-    if (is_plain_vtrace(a)) return launch_kernel<A_, LANES, In, L, true, true, true>(a, st, tiles, vec_tiles, allow_multi);
+    if (is_plain_vtrace(a))
+      return launch_kernel<A_, LANES, In, L, true, true, kPlainCall>(a, st, tiles, vec_tiles, allow_multi);
+    if constexpr (kRewardsPlain) {
+      if (is_plain_vtrace_any_rewards(a))
+        return launch_kernel<A_, LANES, In, L, true, true, kPlainRewards>(a, st, tiles, vec_tiles, allow_multi);
+    }
     return launch_kernel<A_, LANES, In, L, true, true>(a, st, tiles, vec_tiles, allow_multi);
   } else {
     if constexpr (!kFastOnly) {
@@ -682,7 +694,9 @@ int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t ve
   }
 }
 
-template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false>
+// kRewardsPlain: loss calls that are plain V-trace but for a reward transform
+// take the plain kernel too (instantiated for the long-run loss shapes only).
+template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false, bool kRewardsPlain = false>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
   if (kFastOnly && precise_row_sums(a, mode == Mode::LossGrad)) return hipErrorInvalidValue;
   if constexpr (kFastOnly) {
@@ -700,7 +714,7 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
   const int64_t vec_tiles = aligned && offsets32 ? a.B / LANES : 0;
   if constexpr (!kFastOnly) {
     if (mode == Mode::LossGrad) {
-      *nwg = launch_mode<A_, LANES, In, L, true, false>(a, st, tiles, vec_tiles, allow_multi);
+      *nwg = launch_mode<A_, LANES, In, L, true, false, kRewardsPlain>(a, st, tiles, vec_tiles, allow_multi);
       return hipGetLastError();
     }
   }
@@ -800,7 +814,7 @@ bool launch_long(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, boo
 
 // Workgroups of the single-tile loss kernel (plain or with variants) that fit
 // on a compute unit at once, asked of the runtime once (0 if it cannot say).
-template <int A_, int LANES, typename In, int L, bool kPlain>
+template <int A_, int LANES, typename In, int L, int kPlain>
 int loss_workgroups_per_cu() {
   static std::atomic<int> cached{-1};
   int n = cached.load(std::memory_order_relaxed);
@@ -831,12 +845,14 @@ template <int A_, typename In, typename Sh, typename... Rest>
 bool launch_long_loss(const StepArgs& a, hipStream_t st, int64_t* nwg, hipError_t* err, int cus) {
   if (a.B % Sh::LANES == 0) {
     const int64_t tiles = a.B / Sh::LANES;
-    const int per_cu = is_plain_vtrace(a) ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, true>()
-                                          : loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, false>();
+    const int per_cu = is_plain_vtrace(a) ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kPlainCall>()
+                       : is_plain_vtrace_any_rewards(a)
+                           ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kPlainRewards>()
+                           : loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kGeneralCall>();
     const int64_t resident = static_cast<int64_t>(per_cu) * cus;
     if (per_cu * (Sh::LANES * Sh::L / kWave) >= kMinWavesPerCu && resident > 0 && tiles % resident == 0 &&
         tiles <= kMaxGenerations * resident) {
-      *err = launch_shape<A_, Sh::LANES, In, Sh::L>(a, Mode::LossGrad, st, nwg, false);
+      *err = launch_shape<A_, Sh::LANES, In, Sh::L, false, true>(a, Mode::LossGrad, st, nwg, false);
       return true;
     }
   }
