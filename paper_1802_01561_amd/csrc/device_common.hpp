@@ -71,6 +71,11 @@ inline bool is_plain_vtrace_any_rewards(const StepArgs& a) {
   return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs == 0 && a.grad_bf16 == 0;
 }
 
+// The same with behaviour log-probabilities instead of behaviour logits.
+inline bool is_plain_vtrace_log_probs(const StepArgs& a) {
+  return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs != 0 && a.grad_bf16 == 0;
+}
+
 // A call with none of the variants: the above with rewards as given.
 inline bool is_plain_vtrace(const StepArgs& a) { return is_plain_vtrace_any_rewards(a) && a.reward_transform == 0; }
 

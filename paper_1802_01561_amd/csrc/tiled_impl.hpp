@@ -115,11 +115,14 @@ struct Carry {
 };
 
 // Which variant switches a kernel takes at run time: all of them (kGeneralCall),
-// none (kPlainCall: plain V-trace, is_plain_vtrace), or only the reward
-// transform (kPlainRewards: is_plain_vtrace_any_rewards).
+// none (kPlainCall: plain V-trace, is_plain_vtrace), only the reward
+// transform (kPlainRewards: is_plain_vtrace_any_rewards), or only the reward
+// transform with behaviour log-probabilities in place of behaviour logits, so
+// that no behaviour row is read (kPlainLogProbs: is_plain_vtrace_log_probs).
 constexpr int kGeneralCall = 0;
 constexpr int kPlainCall = 1;
 constexpr int kPlainRewards = 2;
+constexpr int kPlainLogProbs = 3;
 
 // Walks one tile (kMulti false: `tile`, with the carry cy set up by the
 // caller), or (kMulti true, vector tiles only) the tiles first_tile + i *
@@ -146,14 +149,15 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
 
   // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
-  // kPlain: the call is plain V-trace (logits of both policies, q_s from
-  // v_{s+1}, float32 gradients), so every variant switch below is a
-  // compile-time constant; kPlainCall also has rewards as given, while
-  // kPlainRewards keeps the reward transform a run-time switch.
+  // kPlain: the call is plain V-trace (q_s from v_{s+1}, float32 gradients,
+  // behaviour logits or, for kPlainLogProbs, log-probabilities), so every
+  // variant switch below is a compile-time constant; kPlainCall also has
+  // rewards as given, while the other plain kernels keep the reward transform
+  // a run-time switch.
   const int correction = kPlain ? kCorrVtrace : a.correction;
   const int q_estimate = kPlain ? 0 : a.q_estimate;
   const int reward_transform = kPlain == kPlainCall ? 0 : a.reward_transform;
-  const bool beh_lp = !kPlain && a.behaviour_log_probs != 0;
+  const bool beh_lp = kPlain == kPlainLogProbs || (!kPlain && a.behaviour_log_probs != 0);
   // No-correction and epsilon-correction never look at the behaviour policy.
   const bool no_ratio = correction == kCorrNone || correction == kCorrEpsilon;
   const bool skip_y = beh_lp || no_ratio;
@@ -674,15 +678,17 @@ int64_t launch_kernel(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t 
 // Loss kernels always take the float64 exponent sums; a targets-only call
 // takes them when its weights can amplify ratio errors.  kFastOnly: only the
 // float32 mode is instantiated (the caller has checked precise_row_sums).
-template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly, bool kRewardsPlain = false>
+template <int A_, int LANES, typename In, int L, bool kGrad, bool kFastOnly, bool kPlainVariants = false>
 int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t vec_tiles,
                     bool allow_multi) {
   if constexpr (kGrad) {
     if (is_plain_vtrace(a))
       return launch_kernel<A_, LANES, In, L, true, true, kPlainCall>(a, st, tiles, vec_tiles, allow_multi);
-    if constexpr (kRewardsPlain) {
+    if constexpr (kPlainVariants) {
       if (is_plain_vtrace_any_rewards(a))
         return launch_kernel<A_, LANES, In, L, true, true, kPlainRewards>(a, st, tiles, vec_tiles, allow_multi);
+      if (is_plain_vtrace_log_probs(a))
+        return launch_kernel<A_, LANES, In, L, true, true, kPlainLogProbs>(a, st, tiles, vec_tiles, allow_multi);
     }
     return launch_kernel<A_, LANES, In, L, true, true>(a, st, tiles, vec_tiles, allow_multi);
   } else {
@@ -694,9 +700,10 @@ int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t ve
   }
 }
 
-// kRewardsPlain: loss calls that are plain V-trace but for a reward transform
-// take the plain kernel too (instantiated for the long-run loss shapes only).
-template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false, bool kRewardsPlain = false>
+// kPlainVariants: loss calls that are plain V-trace but for a reward transform
+// or behaviour log-probabilities take plain kernels too (instantiated for the
+// long-run loss shapes only).
+template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false, bool kPlainVariants = false>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
   if (kFastOnly && precise_row_sums(a, mode == Mode::LossGrad)) return hipErrorInvalidValue;
   if constexpr (kFastOnly) {
@@ -714,7 +721,7 @@ hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* n
   const int64_t vec_tiles = aligned && offsets32 ? a.B / LANES : 0;
   if constexpr (!kFastOnly) {
     if (mode == Mode::LossGrad) {
-      *nwg = launch_mode<A_, LANES, In, L, true, false, kRewardsPlain>(a, st, tiles, vec_tiles, allow_multi);
+      *nwg = launch_mode<A_, LANES, In, L, true, false, kPlainVariants>(a, st, tiles, vec_tiles, allow_multi);
       return hipGetLastError();
     }
   }
@@ -848,6 +855,8 @@ bool launch_long_loss(const StepArgs& a, hipStream_t st, int64_t* nwg, hipError_
     const int per_cu = is_plain_vtrace(a) ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kPlainCall>()
                        : is_plain_vtrace_any_rewards(a)
                            ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kPlainRewards>()
+                       : is_plain_vtrace_log_probs(a)
+                           ? loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kPlainLogProbs>()
                            : loss_workgroups_per_cu<A_, Sh::LANES, In, Sh::L, kGeneralCall>();
     const int64_t resident = static_cast<int64_t>(per_cu) * cus;
     if (per_cu * (Sh::LANES * Sh::L / kWave) >= kMinWavesPerCu && resident > 0 && tiles % resident == 0 &&
