@@ -65,19 +65,22 @@ inline bool ratio_needs_fp64(const Args& a) {
 // targets-only call with every weight at most 1 takes the float32 mode.
 inline bool precise_row_sums(const StepArgs& a, bool losses) { return losses || ratio_needs_fp64(a); }
 
-// A call with none of the variants but possibly a reward transform: V-trace,
-// behaviour logits, q_s from v_{s+1}, float32 gradients.
+// A call with none of the variants but possibly a reward transform and
+// bfloat16 gradients: V-trace, behaviour logits, q_s from v_{s+1}.
 inline bool is_plain_vtrace_any_rewards(const StepArgs& a) {
-  return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs == 0 && a.grad_bf16 == 0;
+  return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs == 0;
 }
 
 // The same with behaviour log-probabilities instead of behaviour logits.
 inline bool is_plain_vtrace_log_probs(const StepArgs& a) {
-  return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs != 0 && a.grad_bf16 == 0;
+  return a.correction == kCorrVtrace && a.q_estimate == 0 && a.behaviour_log_probs != 0;
 }
 
-// A call with none of the variants: the above with rewards as given.
-inline bool is_plain_vtrace(const StepArgs& a) { return is_plain_vtrace_any_rewards(a) && a.reward_transform == 0; }
+// A call with none of the variants: the above with rewards as given and
+// float32 gradients.
+inline bool is_plain_vtrace(const StepArgs& a) {
+  return is_plain_vtrace_any_rewards(a) && a.reward_transform == 0 && a.grad_bf16 == 0;
+}
 
 // The weights a step contributes under a correction variant: rho and c in the
 // value target, and the weight on the advantage.  V-trace uses the truncated

@@ -116,9 +116,9 @@ struct Carry {
 
 // Which variant switches a kernel takes at run time: all of them (kGeneralCall),
 // none (kPlainCall: plain V-trace, is_plain_vtrace), only the reward
-// transform (kPlainRewards: is_plain_vtrace_any_rewards), or only the reward
-// transform with behaviour log-probabilities in place of behaviour logits, so
-// that no behaviour row is read (kPlainLogProbs: is_plain_vtrace_log_probs).
+// transform and the gradient dtype (kPlainRewards: is_plain_vtrace_any_rewards),
+// or those two with behaviour log-probabilities in place of behaviour logits,
+// so that no behaviour row is read (kPlainLogProbs: is_plain_vtrace_log_probs).
 constexpr int kGeneralCall = 0;
 constexpr int kPlainCall = 1;
 constexpr int kPlainRewards = 2;
@@ -149,11 +149,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
 
   // Byte stride of one time row of logits.
   const int64_t in_row = B * A_ * int64_t(sizeof(In));
-  // kPlain: the call is plain V-trace (q_s from v_{s+1}, float32 gradients,
-  // behaviour logits or, for kPlainLogProbs, log-probabilities), so every
-  // variant switch below is a compile-time constant; kPlainCall also has
-  // rewards as given, while the other plain kernels keep the reward transform
-  // a run-time switch.
+  // kPlain: the call is plain V-trace (q_s from v_{s+1}, behaviour logits or,
+  // for kPlainLogProbs, log-probabilities), so every variant switch below is a
+  // compile-time constant; kPlainCall also has rewards as given and float32
+  // gradients, while the other plain kernels keep the reward transform and
+  // the gradient dtype run-time switches.
   const int correction = kPlain ? kCorrVtrace : a.correction;
   const int q_estimate = kPlain ? 0 : a.q_estimate;
   const int reward_transform = kPlain == kPlainCall ? 0 : a.reward_transform;
@@ -161,7 +161,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
   // No-correction and epsilon-correction never look at the behaviour policy.
   const bool no_ratio = correction == kCorrNone || correction == kCorrEpsilon;
   const bool skip_y = beh_lp || no_ratio;
-  const bool grad_bf16 = !kPlain && a.grad_bf16 != 0;
+  const bool grad_bf16 = kPlain != kPlainCall && a.grad_bf16 != 0;
   const int64_t gsz = grad_bf16 ? 2 : 4;  // bytes per gradient element
   const int64_t out_row = B * A_ * gsz;
   const float* const lmu_g = static_cast<const float*>(a.behaviour_logits);
@@ -700,9 +700,9 @@ int64_t launch_mode(const StepArgs& a, hipStream_t st, int64_t tiles, int64_t ve
   }
 }
 
-// kPlainVariants: loss calls that are plain V-trace but for a reward transform
-// or behaviour log-probabilities take plain kernels too (instantiated for the
-// long-run loss shapes only).
+// kPlainVariants: loss calls that are plain V-trace but for a reward
+// transform, bfloat16 gradients or behaviour log-probabilities take plain
+// kernels too (instantiated for the long-run loss shapes only).
 template <int A_, int LANES, typename In, int L = kL, bool kFastOnly = false, bool kPlainVariants = false>
 hipError_t launch_shape(const StepArgs& a, Mode mode, hipStream_t st, int64_t* nwg, bool allow_multi) {
   if (kFastOnly && precise_row_sums(a, mode == Mode::LossGrad)) return hipErrorInvalidValue;

@@ -199,30 +199,33 @@ def test_io_variants_stress_subset():
         check_io_variant(tr, p, log_probs=True, grad_bf16=True, lanes=STRESS_SUBSET)
 
 
-@pytest.mark.parametrize("A,bf16,transform,log_probs,lanes_per_cu",
-                         [(18, False, "clip", False, 64), (18, True, "asymmetric", False, 64),
-                          (9, False, "asymmetric", False, 64), (9, True, "clip", False, 128),
-                          (18, False, None, True, 64), (18, True, "clip", True, 64),
-                          (9, False, "asymmetric", True, 128)])
-def test_plain_kernels_on_long_tiles(A, bf16, transform, log_probs, lanes_per_cu, monkeypatch):
+@pytest.mark.parametrize("A,bf16,transform,log_probs,grad_bf16,lanes_per_cu",
+                         [(18, False, "clip", False, False, 64), (18, True, "asymmetric", False, False, 64),
+                          (9, False, "asymmetric", False, False, 64), (9, True, "clip", False, False, 128),
+                          (18, False, None, True, False, 64), (18, True, "clip", True, False, 64),
+                          (9, False, "asymmetric", True, False, 128), (18, False, None, False, True, 64),
+                          (18, False, "asymmetric", False, True, 64), (9, True, "clip", True, True, 128)])
+def test_plain_kernels_on_long_tiles(A, bf16, transform, log_probs, grad_bf16, lanes_per_cu, monkeypatch):
     """Plain V-trace calls with a reward transform (Atari's clipping, DMLab's
-    asymmetric transform) or with behaviour log-probabilities (what the
-    paper's actors send) on batches that take the long-run loss tiles run
-    plain loss kernels with those as their only switches: sampled lanes
-    against the oracle, and every output against the general kernel of the
-    16-step tiles (VTRACE_KERNEL=tiled_short) within the tolerance."""
+    asymmetric transform), bfloat16 gradients or behaviour log-probabilities
+    (what the paper's actors send) on batches that take the long-run loss
+    tiles run plain loss kernels with those as their only switches: sampled
+    lanes against the oracle, and every output against the general kernel of
+    the 16-step tiles (VTRACE_KERNEL=tiled_short) within the tolerance."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     T, B = 37, lanes_per_cu * cus
     tr = make_random(T, B, A, 6100 + A + lanes_per_cu, noise_std=1.0, end_prob=0.03, bf16=bf16)
     tr.rewards = (tr.rewards * 2.5).astype(np.float32)  # exercise the transform
     p = Params(1.0, 1.0, 1.0)
     lanes = [0, 1, 31, 32, 63, 64, B // 2, B - 33, B - 1]
-    log_case(f"plain kernel on long tiles, rewards {transform} log-probs {log_probs} T={T} B={B} A={A} bf16={bf16}")
+    log_case(f"plain kernel on long tiles, rewards {transform} log-probs {log_probs} bf16 grads {grad_bf16} "
+             f"T={T} B={B} A={A} bf16={bf16}")
     monkeypatch.delenv("VTRACE_KERNEL", raising=False)
-    check_io_variant(tr, p, reward_transform=transform, log_probs=log_probs, lanes=lanes)
+    check_io_variant(tr, p, reward_transform=transform, log_probs=log_probs, grad_bf16=grad_bf16, lanes=lanes)
     dev = to_device(tr)
     kw = dict(rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam, with_vs=True, with_pg_advantages=True,
-              with_lane_losses=True, reward_transform=transform)
+              with_lane_losses=True, reward_transform=transform,
+              grad_dtype=torch.bfloat16 if grad_bf16 else torch.float32)
     if log_probs:
         dev["behaviour_logits"] = torch.from_numpy(behaviour_log_probs(tr)).cuda()
         kw["behaviour"] = "log_probs"
