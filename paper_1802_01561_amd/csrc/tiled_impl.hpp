@@ -311,11 +311,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
     const bool act_ok = act >= 0 && act < A_;
     const int act_c = act_ok ? act : 0;
     if (!act_ok) raise_error_flag(a.error_flag);
-    // e_j and z_j for the gradient.  The plain loss kernels keep both in
-    // registers from the row statistics to the gradient (36 VGPRs that their
-    // two waves per SIMD have), which spares each row two LDS round trips;
-    // the variant kernels, which need those registers for their switches,
-    // take e_j through this thread's row of the gradient staging tile (free
+    // e_j and z_j for the gradient.  The plain loss kernels (every kPlain
+    // mode) keep both in registers from the row statistics to the gradient
+    // (36 VGPRs that their two waves per SIMD have), which spares each row two
+    // LDS round trips; the general kernel, which needs those registers for its
+    // switches, takes e_j through this thread's row of the gradient staging tile (free
     // since the previous chunk's stores, which every thread finished before
     // this chunk's logits barrier), where the gradient row later replaces
     // them, and read z_j again from the logit tile.  The targets-only kernels
