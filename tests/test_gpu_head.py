@@ -21,7 +21,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import (ATOL, RTOL, assert_close, assert_sum_close, head_kappa_hidden, head_kappa_loss,
+from gpu_util import (ATOL, RTOL, assert_close, call_params, f32, assert_sum_close, head_kappa_hidden, head_kappa_loss,
                       head_kappa_param, log_case, np_out, require_gpu)
 from synth import HEAD_WORKLOADS, Params, make_head, make_head_config, subset_head_lanes
 
@@ -71,9 +71,12 @@ def check_head(hb, p, out, *, behaviour_values=None, grad_bf16=False, lanes=None
     beh = sub.behaviour_logits if behaviour_values is None else behaviour_values
     if lanes is not None and behaviour_values is not None:
         beh = behaviour_values[:, lanes]
+    q = call_params(p)
+    if "epsilon" in variant or variant.get("correction") == "epsilon":
+        variant = dict(variant, epsilon=f32(variant.get("epsilon", 1e-6)))
     o = oracle.head_loss_and_grads(sub.hidden, sub.weight, sub.bias, beh, sub.actions,
-                                   sub.rewards, sub.discounts, sub.bootstrap_value, p.rho_bar,
-                                   p.c_bar, p.lam, p.baseline_cost, p.entropy_cost, **variant)
+                                   sub.rewards, sub.discounts, sub.bootstrap_value, q.rho_bar,
+                                   q.c_bar, q.lam, q.baseline_cost, q.entropy_cost, **variant)
     pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
     assert_close("outputs", pick(np_out(out.outputs)), o.outputs)
     assert_close("vs", pick(np_out(out.vs)), o.vs)

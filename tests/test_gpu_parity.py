@@ -12,7 +12,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from gpu_util import assert_close, call_params, log_case, np_out, oracle_args, require_gpu, to_device
 from synth import PARAM_SETS, make_config, make_random, subset_lanes
 from synth.trajectories import STRESS_SUBSET
 
@@ -31,8 +31,9 @@ def check_against_oracle(tr, p, out, lanes=None):
     """Compare every output of a loss_grad call with the oracle (optionally on a
     subset of lanes, where the oracle runs on those lanes alone)."""
     sub = tr if lanes is None else subset_lanes(tr, lanes)
-    o = oracle.loss_and_grads(*oracle_args(sub), p.rho_bar, p.c_bar, p.lam,
-                              p.baseline_cost, p.entropy_cost)
+    q = call_params(p)
+    o = oracle.loss_and_grads(*oracle_args(sub), q.rho_bar, q.c_bar, q.lam,
+                              q.baseline_cost, q.entropy_cost)
     pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
     assert_close("vs", pick(np_out(out.vs)), o.vs)
     assert_close("pg_advantages", pick(np_out(out.pg_advantages)), o.pg_advantages)
@@ -61,7 +62,8 @@ def test_config_matches_oracle(cfg, bf16):
         check_against_oracle(tr, p, out)
         vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
         torch.cuda.synchronize()
-        o = oracle.vtrace(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam)
+        q = call_params(p)
+        o = oracle.vtrace(*oracle_args(tr), q.rho_bar, q.c_bar, q.lam)
         assert_close("targets.vs", np_out(vs), o.vs)
         assert_close("targets.pg_advantages", np_out(pg), o.pg_advantages)
         g = vt.vtrace_gather_logits(dev["target_logits"], dev["behaviour_logits"], dev["actions"])
@@ -111,8 +113,9 @@ def test_stress_every_lane_matches_oracle(stress, pidx):
     o_lane = []
     for l0 in range(0, tr.B, 2048):
         lanes = list(range(l0, min(tr.B, l0 + 2048)))
-        o = oracle.loss_and_grads(*oracle_args(subset_lanes(tr, lanes)), p.rho_bar, p.c_bar, p.lam,
-                                  p.baseline_cost, p.entropy_cost)
+        q = call_params(p)
+        o = oracle.loss_and_grads(*oracle_args(subset_lanes(tr, lanes)), q.rho_bar, q.c_bar, q.lam,
+                                  q.baseline_cost, q.entropy_cost)
         for k, ov in (("vs", o.vs), ("pg_advantages", o.pg_advantages), ("d_values", o.d_values),
                       ("d_logits", o.d_logits)):
             assert_close(f"{k} lanes {l0}..", got[k][:, l0:l0 + len(lanes)], ov)
@@ -622,7 +625,8 @@ def test_two_row_chunks(T, B, A, bf16):
     check_against_oracle(tr, p, run_loss_grad(dev, p))
     vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam)
     torch.cuda.synchronize()
-    ot = oracle.vtrace(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam)
+    q = call_params(p)
+    ot = oracle.vtrace(*oracle_args(tr), q.rho_bar, q.c_bar, q.lam)
     assert_close("targets.vs", np_out(vs), ot.vs)
     assert_close("targets.pg_advantages", np_out(pg), ot.pg_advantages)
     del dev

@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from gpu_util import assert_close, call_params, f32, log_case, np_out, oracle_args, require_gpu, to_device
 from synth import Params, make_config, make_random
 
 pytestmark = pytest.mark.gpu
@@ -32,9 +32,10 @@ def check_variant(tr, p, correction, q_estimate, epsilon=1e-6):
     vs, pg = vt.vtrace_targets(**dev, rho_bar=p.rho_bar, c_bar=p.c_bar, lam=p.lam,
                                correction=correction, q_estimate=q_estimate, epsilon=epsilon)
     torch.cuda.synchronize()
-    o = oracle.loss_and_grads(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
-                              p.entropy_cost, correction=correction, q_estimate=q_estimate,
-                              epsilon=epsilon)
+    q = call_params(p)
+    o = oracle.loss_and_grads(*oracle_args(tr), q.rho_bar, q.c_bar, q.lam, q.baseline_cost,
+                              q.entropy_cost, correction=correction, q_estimate=q_estimate,
+                              epsilon=f32(epsilon))
     tag = f"{correction}/{q_estimate}"
     assert_close(f"{tag} vs", np_out(out.vs), o.vs)
     assert_close(f"{tag} pg_advantages", np_out(out.pg_advantages), o.pg_advantages)
@@ -143,9 +144,10 @@ def check_io_variant(tr, p, *, log_probs=False, reward_transform=None, grad_bf16
     if lanes is not None:
         idx = np.asarray(lanes)
         otr_args = [x[:, idx] if i != 6 else x[idx] for i, x in enumerate(otr_args)]
-    o = oracle.loss_and_grads(*otr_args, p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
-                              p.entropy_cost, correction=correction, q_estimate=q_estimate,
-                              behaviour=behaviour, reward_transform=reward_transform)
+    q = call_params(p)
+    o = oracle.loss_and_grads(*otr_args, q.rho_bar, q.c_bar, q.lam, q.baseline_cost,
+                              q.entropy_cost, correction=correction, q_estimate=q_estimate,
+                              behaviour=behaviour, reward_transform=reward_transform, epsilon=f32(1e-6))
     pick = (lambda x: x) if lanes is None else (lambda x: x[:, lanes])
     tag = f"lp={log_probs} r={reward_transform} bf16={grad_bf16} {correction}/{q_estimate}"
     assert_close(f"{tag} vs", pick(np_out(out.vs)), o.vs)

@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import paper_1802_01561_amd as vt
-from gpu_util import assert_close, log_case, np_out, oracle_args, require_gpu, to_device
+from gpu_util import assert_close, call_params, log_case, np_out, oracle_args, require_gpu, to_device
 from synth import PARAM_SETS, make_config, make_random
 
 pytestmark = pytest.mark.gpu
@@ -43,8 +43,9 @@ def test_static_entry_matches_workspace_entry_twice():
         torch.cuda.synchronize()
         for name in ("losses", "d_logits", "d_values", "vs", "pg_advantages", "lane_losses"):
             _same_bits(name, getattr(out, name), getattr(ref, name))
-        o = oracle.loss_and_grads(*oracle_args(tr), p.rho_bar, p.c_bar, p.lam, p.baseline_cost,
-                                  p.entropy_cost)
+        q = call_params(p)
+        o = oracle.loss_and_grads(*oracle_args(tr), q.rho_bar, q.c_bar, q.lam, q.baseline_cost,
+                                  q.entropy_cost)
         assert_close("vs", np_out(out.vs), o.vs)
         assert_close("pg_advantages", np_out(out.pg_advantages), o.pg_advantages)
         assert_close("d_logits", np_out(out.d_logits), o.d_logits)
