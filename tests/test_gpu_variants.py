@@ -277,6 +277,20 @@ def _sweep_cases():
         cases.append(dict(T=37, B=16384, A=A, bf16=bf16, p=Params(1.0, 0.5, 0.95), correction=corr,
                           q_estimate=qe, log_probs=lp, reward_transform=rt, grad_bf16=gb,
                           lanes=[0, 1, 31, 32, 63, 64, 8191, 16320, 16383]))
+    # around the crossover between the time-parallel and the tiled kernel
+    # (T from 17 to 256, B from 8 to 1024) and with lambda = 0.95, whose
+    # float32 value the call receives
+    for _ in range(12):
+        cases.append(dict(
+            T=int(rng.choice([17, 20, 48, 100, 129, 200, 256])),
+            B=int(rng.choice([8, 15, 100, 512, 700, 1024])),
+            A=int(rng.choice([9, 18])),
+            bf16=bool(rng.random() < 0.3),
+            p=Params(float(rng.choice([1.0, math.inf])), float(rng.choice([1.0, 0.5, math.inf])), 0.95),
+            correction=str(rng.choice(["vtrace", "vtrace", "none", "one_step_is"])),
+            q_estimate=str(rng.choice(Q_ESTIMATES)), log_probs=bool(rng.random() < 0.4),
+            reward_transform=rng.choice([None, "clip", "asymmetric"]), grad_bf16=bool(rng.random() < 0.3),
+            lanes=None))
     # 128 lanes per CU: loss calls with A = 9 take 64 x 4 tiles
     for bf16, lp, gb, corr, qe in [(False, True, False, "epsilon", "vtrace"), (True, False, True, "one_step_is", "baseline")]:
         cases.append(dict(T=21, B=32768, A=9, bf16=bf16, p=Params(2.0, 1.0, 0.9), correction=corr,
@@ -294,7 +308,8 @@ def test_random_sweep(i):
     once, which take the tiled kernel's multi-tile walk (bf16 logits with
     A = 9: the 32 x 8 long-run tiles, which fill the chip once there), of
     16384 lanes, which take the long-run tile shapes, and of 32768 lanes with
-    A = 9, whose loss calls take 64 x 4 tiles."""
+    A = 9, whose loss calls take 64 x 4 tiles; and draws around the crossover
+    between the time-parallel and the tiled kernel with lambda = 0.95."""
     c = _sweep_cases()[i]
     tr = make_random(c["T"], c["B"], c["A"], 900 + i, noise_std=1.0, end_prob=0.03, bf16=c["bf16"])
     tr.rewards = (tr.rewards * 2.5).astype(np.float32)  # exercise the clipping
