@@ -497,10 +497,16 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         }
       });
       if (step_ok && g == 0) {
-        const double log_pa =
-            !act_ok ? NAN
-            : eps_mode ? static_cast<double>(logf(pa + a.epsilon))
-                       : static_cast<double>(za - mz) - static_cast<double>(log_s);
+        // log pi(a), and for the epsilon-correction log(pi(a) + eps) as the
+        // float64 log-sum of log pi(a) and log eps: pi(a) + eps rounded to
+        // float32 would lose eps near pi(a) = 1 (1 + 1e-6 is 1.00000095 there).
+        const double lp = static_cast<double>(za - mz) - static_cast<double>(log_s);
+        double log_pa = lp;
+        if (eps_mode) {
+          const double le = log(static_cast<double>(a.epsilon));
+          log_pa = lp >= le ? lp + log1p(exp(le - lp)) : le + log1p(exp(lp - le));
+        }
+        if (!act_ok) log_pa = NAN;
         l_pg += -adv * log_pa;
         l_base += 0.5 * A_t * A_t;
         l_ent += -static_cast<double>(Hent);

@@ -150,6 +150,22 @@ def test_head_correction_variants(correction, q_estimate):
         check_head(hb, p, out, correction=correction, q_estimate=q_estimate)
 
 
+@pytest.mark.parametrize("H", [64, 256])
+def test_head_epsilon_correction_with_a_certain_action(H):
+    """The epsilon-correction with a single action, where pi(a) = 1: every
+    policy-gradient term is -adv log(1 + eps), about -adv eps, and their sums
+    must still meet the bound; pi(a) + eps rounded to float32 (1.00000095 for
+    eps = 1e-6) would be 5% off in every term."""
+    A = 1
+    hb = make_head(40, 33, A, H, 4100 + H, end_prob=0.05)
+    hb.rewards = (hb.rewards * 2.5).astype(np.float32)
+    dev = head_to_device(hb)
+    for p in (Params(1.0, math.inf, 0.95), Params(1.0, 1.0, 1.0)):
+        log_case(f"head epsilon-correction A={A} H={H} {p.label()}")
+        out = run_head(dev, p, correction="epsilon", reward_transform="asymmetric")
+        check_head(hb, p, out, correction="epsilon", reward_transform="asymmetric")
+
+
 @pytest.mark.parametrize("log_probs", [False, True])
 @pytest.mark.parametrize("reward_transform", [None, "asymmetric"])
 @pytest.mark.parametrize("grad_bf16", [False, True])
