@@ -188,6 +188,47 @@ def test_head_io_variants(log_probs, reward_transform, grad_bf16):
         check_head(hb, p, out, behaviour_values=beh_vals, grad_bf16=grad_bf16, **kw)
 
 
+def _head_sweep_cases():
+    """Seeded draws over the output-layer call's axes: shapes (one or two
+    column tiles, each hidden size, ragged T and B, a single action),
+    clipping levels, corrections and Q estimates, behaviour log-probabilities,
+    reward transforms and bf16 d_hidden."""
+    rng = np.random.default_rng(20261203)
+    cases = []
+    for _ in range(16):
+        cases.append(dict(
+            T=int(rng.choice([1, 5, 16, 17, 31, 40])), B=int(rng.choice([1, 3, 4, 7, 16, 33])),
+            A=int(rng.choice([1, 5, 9, 15, 16, 18, 31])), H=int(rng.choice([64, 128, 256])),
+            p=Params(float(rng.choice([1.0, math.inf, 2.0])), float(rng.choice([1.0, 0.5, math.inf])),
+                     float(rng.choice([1.0, 0.95]))),
+            log_probs=bool(rng.random() < 0.3), reward_transform=rng.choice([None, "clip", "asymmetric"]),
+            grad_bf16=bool(rng.random() < 0.3),
+            correction=str(rng.choice(["vtrace", "vtrace", "none", "epsilon", "one_step_is"])),
+            q_estimate=str(rng.choice(["vtrace", "baseline"]))))
+    return cases
+
+
+@pytest.mark.parametrize("i", range(len(_head_sweep_cases())))
+def test_head_random_sweep(i):
+    """Each seeded draw against the oracle (every output, d_W, d_b and the
+    loss totals)."""
+    c = _head_sweep_cases()[i]
+    hb = make_head(c["T"], c["B"], c["A"], c["H"], 20000 + i, end_prob=0.05)
+    hb.rewards = (hb.rewards * 2.5).astype(np.float32)
+    beh_vals = None
+    if c["log_probs"]:
+        import scipy.special
+        lp = scipy.special.log_softmax(hb.behaviour_logits.astype(np.float64), axis=-1)
+        beh_vals = np.take_along_axis(lp, hb.actions[..., None].astype(np.int64), -1)[..., 0]
+        beh_vals = beh_vals.astype(np.float32)
+    dev = head_to_device(hb, behaviour=beh_vals)
+    kw = dict(behaviour="log_probs" if c["log_probs"] else "logits", reward_transform=c["reward_transform"],
+              correction=c["correction"], q_estimate=c["q_estimate"])
+    log_case(f"head sweep {i}: " + ", ".join(f"{k}={v}" for k, v in c.items()))
+    out = run_head(dev, c["p"], grad_dtype=torch.bfloat16 if c["grad_bf16"] else torch.float32, **kw)
+    check_head(hb, c["p"], out, behaviour_values=beh_vals, grad_bf16=c["grad_bf16"], **kw)
+
+
 def test_head_bf16_behaviour_logits():
     from synth import bf16_bits_to_f32, f32_to_bf16_bits
     hb = make_head(33, 8, 9, 256, 32)
