@@ -270,15 +270,25 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       g32 = p_g;
       V32 = p_V;
       lmu = p_lmu;
-      __syncthreads();
-      if constexpr (kMulti) {
-        if (it + 1 < total) {
-          const bool next_tile = k + 1 == nchunks;
-          prefetch(next_tile ? tile + tile_stride : tile, next_tile ? 0 : k + 1);
+      // The next chunk's loads go out before the staging barrier (their
+      // registers are free once staged) with float32 logits on the long-run
+      // shapes: stress step 0.730 -> 0.714 ms, bf16 gradients 0.682 -> 0.670,
+      // targets-only 0.550 -> 0.537; with bf16 logits and on the 16-step tiles
+      // they measured 1% slower and stay after it.
+      constexpr bool kEarlyPrefetch = std::is_same_v<In, float> && L <= 8;
+      auto next_prefetch = [&]() {
+        if constexpr (kMulti) {
+          if (it + 1 < total) {
+            const bool next_tile = k + 1 == nchunks;
+            prefetch(next_tile ? tile + tile_stride : tile, next_tile ? 0 : k + 1);
+          }
+        } else {
+          if (k + 1 < nchunks) prefetch(tile, k + 1);
         }
-      } else {
-        if (k + 1 < nchunks) prefetch(tile, k + 1);
-      }
+      };
+      if constexpr (kEarlyPrefetch) next_prefetch();
+      __syncthreads();
+      if constexpr (!kEarlyPrefetch) next_prefetch();
     } else {
       In* lz = reinterpret_cast<In*>(lds_z);
       In* ly = reinterpret_cast<In*>(lds_y);
