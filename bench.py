@@ -445,7 +445,7 @@ def main():
     import torch
 
     import paper_1802_01561_amd as vt
-    from synth import PARAM_SETS, make_config
+    from synth import PARAM_SETS, WORKLOADS, make_config
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -487,8 +487,8 @@ def main():
         flush = lambda: flush_buf.fill_(1)  # noqa: E731
     kernel_ms, ms_per_step = timed_calls(step, K, args.warmup, stream, flush)
     main_losses = out.losses.clone()  # on the stream: the sets below reuse `out`
-    is_counted_workload = (args.config == 4 and args.params == 0 and not args.bf16
-                           and args.kernel == "auto" and args.correction == "vtrace"
+    is_counted_workload = (WORKLOADS[args.config]["name"] == "stress" and args.params == 0
+                           and not args.bf16 and args.kernel == "auto" and args.correction == "vtrace"
                            and not args.log_probs and not args.grad_bf16
                            and args.reward_transform is None)
     # The stress batch's other parameter sets on the same inputs, timed right
