@@ -285,12 +285,12 @@ def timed_calls(step, K, W, stream, flush=None):
     return np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]), (t1 - t0) * 1e3 / K
 
 
-def head_algorithmic_bytes(T, B, A, H, grad_bytes):
+def head_algorithmic_bytes(T, B, A, H, grad_bytes, log_probs=False):
     """Bytes the fused output-layer call must move: per step the hidden row
-    (bfloat16), the behaviour logit row, action, reward and discount in and the
-    d_hidden row out; per call the bootstrap values, the layer's parameters in
-    and their gradients out."""
-    per_step = 2 * H + 4 * A + 12 + grad_bytes * H
+    (bfloat16), the behaviour logit row (or log mu(a_t|x_t)), action, reward and
+    discount in and the d_hidden row out; per call the bootstrap values, the
+    layer's parameters in and their gradients out."""
+    per_step = 2 * H + (4 if log_probs else 4 * A) + 12 + grad_bytes * H
     per_call = 4 * B + (2 * H * (A + 1) + 4 * (A + 1)) + (4 * H * (A + 1) + 4 * (A + 1) + 16)
     return T * B * per_step + per_call, per_step
 
@@ -353,6 +353,13 @@ def run_head(args):
           f"(generated on the device in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr,
           flush=True)
     grad_dtype = torch.bfloat16 if args.grad_bf16 else torch.float32
+    beh, behaviour = d["behaviour_logits"], "logits"
+    if args.log_probs:
+        # log mu(a_t|x_t), computed once on the device outside the timed region
+        lp = torch.log_softmax(beh, dim=-1)
+        beh = lp.gather(-1, d["actions"].long()[..., None])[..., 0].contiguous()
+        del lp
+        behaviour = "log_probs"
     ws = vt.Workspace(T, B, A, H=H)
     f32 = dict(dtype=torch.float32, device="cuda")
     out = vt.HeadLossGrad(torch.empty(4, **f32), torch.empty((T, B, H), dtype=grad_dtype, device="cuda"),
@@ -361,22 +368,22 @@ def run_head(args):
     stream = torch.cuda.current_stream()
 
     def step():
-        vt.vtrace_head_loss_grad(d["hidden"], d["weight"], d["bias"], d["behaviour_logits"],
+        vt.vtrace_head_loss_grad(d["hidden"], d["weight"], d["bias"], beh,
                                  d["actions"], d["rewards"], d["discounts"], d["bootstrap_value"],
                                  p.rho_bar, p.c_bar, p.lam, p.baseline_cost, p.entropy_cost,
-                                 workspace=ws, out=out, grad_dtype=grad_dtype)
+                                 workspace=ws, out=out, grad_dtype=grad_dtype, behaviour=behaviour)
 
     call_ms, ms_per_step = timed_calls(step, args.steps, args.warmup, stream)
     avg_ms = float(call_ms.mean())
     grad_bytes = 2 if args.grad_bf16 else 4
-    alg_bytes, per_step = head_algorithmic_bytes(T, B, A, H, grad_bytes)
+    alg_bytes, per_step = head_algorithmic_bytes(T, B, A, H, grad_bytes, args.log_probs)
     achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
     mfma_flop = 3 * 2 * T * B * H * (A + 1)  # forward, d_hidden, d_weight
     print(f"[bench] head call avg {avg_ms:.4f} ms (min {call_ms.min():.4f}); wall "
           f"{ms_per_step:.4f} ms/step; {achieved:.1f} GB/s algorithmic; "
           f"{mfma_flop / (avg_ms * 1e-3) / 1e12:.1f} TFLOP/s of matrix products; losses "
           f"{out.losses.cpu().tolist()}", file=sys.stderr, flush=True)
-    counted = not args.grad_bf16
+    counted = not args.grad_bf16 and not args.log_probs
     traffic, traffic_bytes = (stored_traffic(avg_ms, HEAD_COUNTERS_FILE, HEAD_SOURCES) if counted
                               else (None, None))
     result = {
@@ -394,7 +401,8 @@ def run_head(args):
         "data": "synthetic",
         "config": {
             "workload": f"stress + output layer: T={T} B={B} A={A} H={H}, bf16 hidden and "
-                        f"weights, f32 behaviour logits, {'bf16' if args.grad_bf16 else 'f32'} "
+                        f"weights, f32 behaviour {'log-probabilities' if args.log_probs else 'logits'}, "
+                        f"{'bf16' if args.grad_bf16 else 'f32'} "
                         f"d_hidden, rho_bar=c_bar=lambda=1",
             "T": T, "B": B, "A": A, "H": H, "seed": seed,
         },

@@ -32,6 +32,8 @@ def test_head_call_bytes():
     assert bench.head_algorithmic_bytes(10, 3, 18, 256, 2)[1] == 1108
     per_call = 4 * 3 + (2 * 256 * 19 + 4 * 19) + (4 * 256 * 19 + 4 * 19 + 16)
     assert bench.head_algorithmic_bytes(10, 3, 18, 256, 2)[0] == 10 * 3 * 1108 + per_call
+    # log mu(a_t|x_t) [T,B] in place of mu's logit row
+    assert bench.head_algorithmic_bytes(10, 3, 18, 256, 4, log_probs=True)[1] == 1620 - 4 * 18 + 4
 
 
 def test_digest_follows_the_kernel_sources(tmp_path, monkeypatch):
