@@ -276,6 +276,12 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       // targets-only 0.550 -> 0.537; with bf16 logits and on the 16-step tiles
       // they measured 1% slower and stay after it.
       constexpr bool kEarlyPrefetch = std::is_same_v<In, float> && L <= 8;
+      // The wave issues those loads at raised priority, so that the other
+      // waves' arithmetic on the same SIMD does not delay them: stress step
+      // 0.727-0.730 -> 0.714-0.716 ms, 16-step tiles with float32 logits and
+      // bf16 logits on the long-run shapes 1-2% faster; bf16 logits on the
+      // 16-step tiles measured 1% slower with it and keep normal priority.
+      constexpr bool kPrioPrefetch = std::is_same_v<In, float> || L <= 8;
       auto next_prefetch = [&]() {
         if constexpr (kMulti) {
           if (it + 1 < total) {
@@ -286,9 +292,14 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
           if (k + 1 < nchunks) prefetch(tile, k + 1);
         }
       };
-      if constexpr (kEarlyPrefetch) next_prefetch();
+      auto issue_prefetch = [&]() {
+        if constexpr (kPrioPrefetch) __builtin_amdgcn_s_setprio(2);
+        next_prefetch();
+        if constexpr (kPrioPrefetch) __builtin_amdgcn_s_setprio(0);
+      };
+      if constexpr (kEarlyPrefetch) issue_prefetch();
       __syncthreads();
-      if constexpr (!kEarlyPrefetch) next_prefetch();
+      if constexpr (!kEarlyPrefetch) issue_prefetch();
     } else {
       In* lz = reinterpret_cast<In*>(lds_z);
       In* ly = reinterpret_cast<In*>(lds_y);
@@ -439,6 +450,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
         const int neg = t0 < 0 ? static_cast<int>(-t0) : 0;
         const gptr<char> dgr = offset_bytes(a.d_logits, row0 * A_ * gsz);  // the chunk's row 0
         if (!grad_bf16) {
+          // The kernel that reads no behaviour rows spends a larger share of
+          // each chunk on these stores; issued at raised priority its stress
+          // step took 0.528-0.530 -> 0.519-0.522 ms (the default kernel's
+          // measured 0.4% slower with it).
+          if constexpr (kPlain == kPlainLogProbs) __builtin_amdgcn_s_setprio(2);
           static_for<S::NO>([&](auto I) {
             constexpr int i = decltype(I)::value;
             const int f = tid + i * NT;
@@ -451,6 +467,7 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
                                                   static_cast<uint32_t>(cc) * 16u)));
             }
           });
+          if constexpr (kPlain == kPlainLogProbs) __builtin_amdgcn_s_setprio(0);
         } else {
           // bfloat16 rows: each 16-byte store packs two 16-byte LDS vectors.
           constexpr int kRow16 = S::OUT_ROW16 / 2, kTile16 = S::OUT_TILE16 / 2;
