@@ -338,7 +338,15 @@ __global__ __launch_bounds__(kHeadThreads, 2) void head_kernel(HeadArgs a) {
         });
         sy = group_sum(syl);
       }
-      if (k + 1 < nchunks) prefetch(k + 1);
+      // The next chunk's loads go out at raised wave priority, ahead of the
+      // other wave's matrix products on the same SIMD: 6.64-6.65 -> 6.25-6.26
+      // ms at the stress shape with float32 d_hidden; with bf16 d_hidden it
+      // measured 0.6% slower and keeps normal priority.
+      if (k + 1 < nchunks) {
+        if constexpr (!kBf16Grad) __builtin_amdgcn_s_setprio(2);
+        prefetch(k + 1);
+        if constexpr (!kBf16Grad) __builtin_amdgcn_s_setprio(0);
+      }
 
       // 2. Epilogue.
       r32 = transform_reward(r32, a.reward_transform);
