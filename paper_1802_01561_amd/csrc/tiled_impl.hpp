@@ -273,10 +273,11 @@ __device__ __forceinline__ void chunk_walk(const StepArgs& a, v4u* lds, int64_t 
       // The next chunk's loads go out before the staging barrier (their
       // registers are free once staged) with float32 logits on the long-run
       // shapes: stress step 0.730 -> 0.714 ms, bf16 gradients 0.682 -> 0.670,
-      // targets-only 0.550 -> 0.537.  With bf16 logits only the kernel that
-      // reads no behaviour rows gains (0.485-0.491 -> 0.466-0.468 ms, with
-      // bf16 gradients 0.453-0.455 -> 0.432-0.433); the others, and the
-      // 16-step tiles, measured up to 1% slower and keep them after it.
+      // targets-only 0.550 -> 0.537.  With bf16 logits (and the raised
+      // priority below) only the kernel that reads no behaviour rows gains
+      // (0.485-0.491 -> 0.466-0.468 ms, with bf16 gradients 0.453-0.455 ->
+      // 0.432-0.433); the others, and the 16-step tiles, measured up to 1%
+      // slower and keep them after it.
       constexpr bool kEarlyPrefetch =
           L <= 8 && (std::is_same_v<In, float> || kPlain == kPlainLogProbs);
       // The wave issues those loads at raised priority, so that the other
